@@ -1,0 +1,183 @@
+"""Decode-attention benchmark on one MI355X.
+
+One step = one whole decode-attention call (plan + attention + combine) over
+the chat-like batch: 256 requests, 32 query / 8 KV heads, head_dim 128,
+lengths lognormal (median 1200, sigma 0.8) clipped to [16, 16384], 16-token
+pages in shuffled order, bf16 N(0,1) values, seed 0 (synthetic; stands in for
+chat-trace length mixes).  Inputs are resident in HBM before timing starts.
+
+Prints one JSON line:
+  value         KV bytes per step / step time, GB/s (whole job, all N GPUs)
+  ms_per_step   wall time per step from events around the K timed steps
+  roofline      the attention kernel: algorithmic bytes per launch / its
+                average launch time (HIP events on the launch stream) against
+                MI355X's 8 TB/s; traffic from the committed FETCH_SIZE /
+                WRITE_SIZE counter summary when it matches this kernel source
+  cpu_baseline  the fp64 oracle on the host cores over the same workload
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+WORKLOAD = "chat_b256"
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in ("paper_2509_04827_amd/csrc/vdecode.hip", "include/vdecode.h",
+                "paper_2509_04827_amd/build.py"):
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic(workload: str):
+    """HBM bytes per attention launch from profiles/, if taken on this source."""
+    path = os.path.join(ROOT, "profiles", "attn_kernel_%s_traffic.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="stop repeating the oracle after this much wall time")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures one GPU; the decode-attention path has no "
+              "multi-GPU mode (sequences shard across GPUs with no exchange). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2509_04827_amd as vd
+    from workloads import WORKLOADS, bits, kv_bytes, make_case
+
+    w = WORKLOADS[args.workload]
+    t0 = time.time()
+    c = make_case(w, seed=0, fill="zero")
+    print("bench: %s generated in %.1fs: N_req %d N_kv %d pages %d"
+          % (w.name, time.time() - t0, c["num_seqs"], c["n_kv"], c["num_pages"]),
+          file=sys.stderr, flush=True)
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    q = c["q"].to(dev)
+    k = c["k_pages"].to(dev)
+    v = c["v_pages"].to(dev)
+    pt = c["page_table"].to(dev)
+    sl = c["seq_lens"].to(dev)
+    out = torch.empty(q.shape, dtype=torch.bfloat16, device=dev)
+    B, Hq, Hkv, maxp = c["num_seqs"], c["n_q_heads"], c["n_kv_heads"], c["max_pages_per_seq"]
+    ws = vd.alloc_workspace(B, Hq, Hkv, maxp)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step(ev0=None, ev1=None):
+        vd.vd_decode_plan(sl, Hq, Hkv, maxp, ws, stream=stream)
+        if ev0 is not None:
+            ev0.record(stream)
+        vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws, stream=stream)
+        if ev1 is not None:
+            ev1.record(stream)
+        vd.vd_decode_combine(out, Hkv, maxp, ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    a0 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    a1 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(K):
+        step(a0[i], a1[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / K
+    attn_ms = [a0[i].elapsed_time(a1[i]) for i in range(K)]
+    attn_avg_ms = float(np.mean(attn_ms))
+
+    kvb = kv_bytes(c)
+    P = (c["seq_lens"].numpy().astype(np.int64) + 15) // 16
+    algo_bytes = (kvb + q.numel() * 2 + out.numel() * 2 + int(P.sum()) * 4 + B * 4)
+    achieved = algo_bytes / (attn_avg_ms * 1e-3) / 1e9
+    value = kvb / (ms_step * 1e-3) / 1e9
+    traffic = committed_traffic(w.name)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        hq, hk, hv = bits(c["q"]), bits(c["k_pages"]), bits(c["v_pages"])
+        hpt, hsl = c["page_table"].numpy(), c["seq_lens"].numpy()
+        times = []
+        t_end = time.time() + args.cpu_seconds
+        while True:
+            t1 = time.time()
+            oracle.decode_attn(hq, hk, hv, hpt, hsl, c["scale"])
+            times.append(time.time() - t1)
+            if time.time() >= t_end or len(times) >= 5:
+                break
+        sec = float(np.median(times))
+        cpu = {"value": round(kvb / sec / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
+               "kind": "oracle",
+               "sample": "the whole %s step (all %d requests, %d KV tokens), fp64, %d run(s), "
+                         "median %.2f s" % (w.name, B, c["n_kv"], len(times), sec)}
+
+    line = {
+        "metric": "decode-attention achieved HBM GB/s (% of peak) and us/step vs batch x KV tokens",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "us_per_step": round(ms_step * 1e3, 2),
+        "pct_of_peak": round(100.0 * value / PEAK_HBM_GBS, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "description": w.description, "num_seqs": B,
+                   "n_q_heads": Hq, "n_kv_heads": Hkv, "head_dim": 128, "page_size": 16,
+                   "n_kv_tokens": c["n_kv"], "kv_bytes": kvb, "seed": 0},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "traffic": traffic, "kernel": "attn_kernel",
+                     "algorithmic_bytes": algo_bytes, "avg_launch_us": round(attn_avg_ms * 1e3, 2)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,156 @@
+/*
+ * vdecode.h -- libvdecode: batched single-token GQA decode attention over a
+ * paged KV cache, for AMD Instinct MI355X (gfx950).
+ *
+ * The operation.  A decode iteration of a served model attends the newest
+ * query token of each of N_req running requests to the N_kv tokens cached for
+ * it; the paper models the iteration's attention work and KV-cache reads as
+ * growing with N_kv (EcoPred, Sec. 5.4, Eq. pred-itl), with the cache held in
+ * fixed-size pages (PagedAttention, Sec. 2.1).  For request b holding L_b
+ * cached tokens and query head h (G = n_q_heads / n_kv_heads, g = h / G):
+ *     s_t    = scale * <q[b][h], k_t>              for t = 0 .. L_b - 1
+ *     out[b][h] = sum_t softmax(s)_t * v_t
+ * with k_t, v_t = row (t mod page_size) of physical page
+ * page_table[b][t / page_size], KV head g.  L_b = 0 gives out = 0.
+ * The result is plain softmax attention: no causal mask (every cached token,
+ * the current one included, is attended), no window, no soft-cap.
+ *
+ * Layouts (row-major, element sizes in brackets):
+ *   q          bf16  [num_seqs][n_q_heads][head_dim]
+ *   k_pages    bf16  [num_pages][page_size][n_kv_heads][head_dim]
+ *   v_pages    bf16  same as k_pages
+ *   page_table int32 [num_seqs][max_pages_per_seq]   entries >= ceil(L_b/page_size) unused
+ *   seq_lens   int32 [num_seqs]   L_b, cached tokens including the current one
+ *   out        bf16 (default) or fp32 (VD_FLAG_OUT_F32) [num_seqs][n_q_heads][head_dim]
+ *
+ * Supported shapes: head_dim = 128, page_size = 16,
+ * G in {1, 2, 4, 8, 16}, 0 <= num_seqs <= 8192.
+ *
+ * Conventions for every call:
+ *   - Pointers are device pointers owned by the caller; the library never
+ *     allocates, frees or synchronises, and keeps no global state, so calls
+ *     from several threads are safe.  Concurrent calls need distinct
+ *     workspaces.  out must not alias an input.
+ *   - q, k_pages, v_pages, out, k_out, v_out and workspace must be 16-byte
+ *     aligned; page_table and seq_lens 4-byte aligned.
+ *   - Work is enqueued on `stream` and the call returns at once.
+ *   - Argument errors are found on the host before anything is enqueued and
+ *     return a nonzero vd_status; VD_ERROR_LAUNCH reports a failed launch.
+ *   - Device-resident data is not validated: 0 <= L_b and every page id a
+ *     request uses is a valid page of the pools are preconditions.  L_b larger
+ *     than max_pages_per_seq * page_size is clamped to it.
+ *   - bf16 inputs are read as stored; arithmetic is fp32; bf16 outputs are
+ *     rounded to nearest even.
+ */
+#ifndef VDECODE_H
+#define VDECODE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum vd_status {
+    VD_SUCCESS = 0,
+    VD_ERROR_INVALID_VALUE = 1,       /* NULL pointer, bad size, misalignment, bad flag, non-finite scale */
+    VD_ERROR_NOT_SUPPORTED = 2,       /* head_dim, page_size, G or num_seqs outside the supported set */
+    VD_ERROR_WORKSPACE_TOO_SMALL = 3, /* workspace_bytes below vd_decode_workspace_size() */
+    VD_ERROR_LAUNCH = 4               /* a kernel launch failed (hipGetLastError) */
+} vd_status;
+
+/* flags */
+#define VD_FLAG_OUT_F32 (1u << 0)     /* out is fp32 instead of bf16 */
+/* bits 8..15: force the split size to this many pages (1..64); 0 = automatic.
+ * For tests of split invariance; the workspace must hold the resulting plan. */
+#define VD_FLAG_SPLIT_SHIFT 8u
+#define VD_FLAG_SPLIT_MASK (0xFFu << VD_FLAG_SPLIT_SHIFT)
+#define VD_FLAG_SPLIT_PAGES(n) (((unsigned)(n) & 0xFFu) << VD_FLAG_SPLIT_SHIFT)
+
+/* Human-readable name of a vd_status value; never NULL. */
+const char *vd_status_string(int status);
+
+/*
+ * Bytes of device workspace a call with these sizes needs: the split plan and
+ * the split partials (per split and query head: running max, normaliser and an
+ * fp32 head_dim accumulator).  Independent of the actual lengths; grows with
+ * num_seqs * max_pages_per_seq only for very large caches.  `flags` as passed
+ * to the attention call: a forced split size (VD_FLAG_SPLIT_PAGES) can need
+ * more room than the automatic plan.  Returns 0 when the sizes or flags are
+ * invalid or unsupported.
+ */
+size_t vd_decode_workspace_size(int num_seqs, int n_q_heads, int n_kv_heads,
+                                int head_dim, int page_size,
+                                int max_pages_per_seq, unsigned flags);
+
+/*
+ * The whole decode-attention step: vd_decode_plan, vd_decode_partial and
+ * vd_decode_combine enqueued back to back on `stream`.
+ * scale: the softmax scale applied to q.k (1/sqrt(head_dim) for standard
+ * attention); must be finite.
+ */
+int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
+                   const int32_t *page_table, const int32_t *seq_lens,
+                   void *out, int num_seqs, int n_q_heads, int n_kv_heads,
+                   int head_dim, int page_size, float scale,
+                   int max_pages_per_seq, void *workspace,
+                   size_t workspace_bytes, unsigned flags, hipStream_t stream);
+
+/*
+ * Stage 1 of 3: split every request's page range into load-balanced chunks
+ * (one work item per chunk and KV head) and write the plan into the
+ * workspace.  Depends only on seq_lens and the sizes, so one plan serves
+ * every layer of a decode step.
+ */
+int vd_decode_plan(const int32_t *seq_lens, int num_seqs, int n_q_heads,
+                   int n_kv_heads, int head_dim, int page_size,
+                   int max_pages_per_seq, void *workspace,
+                   size_t workspace_bytes, unsigned flags, hipStream_t stream);
+
+/*
+ * Stage 2 of 3: attention over every work item of the plan in `workspace`.
+ * Requests that fit in one chunk get their final output here; the others
+ * leave per-chunk partials in the workspace.  Arguments as vd_decode_attn;
+ * seq_lens, the sizes and flags must match the plan's.
+ */
+int vd_decode_partial(const void *q, const void *k_pages, const void *v_pages,
+                      const int32_t *page_table, const int32_t *seq_lens,
+                      void *out, int num_seqs, int n_q_heads, int n_kv_heads,
+                      int head_dim, int page_size, float scale,
+                      int max_pages_per_seq, void *workspace,
+                      size_t workspace_bytes, unsigned flags,
+                      hipStream_t stream);
+
+/*
+ * Stage 3 of 3: log-sum-exp merge of the partials of every request that was
+ * split, and zeros for requests with L_b = 0.  Sizes and flags as the plan's.
+ */
+int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads,
+                      int head_dim, int page_size, int max_pages_per_seq,
+                      void *workspace, size_t workspace_bytes, unsigned flags,
+                      hipStream_t stream);
+
+/*
+ * Copy-through check of the gather: plans like vd_decode_attn, runs the
+ * attention kernel's own page-table walk, K/V loads, tail masking and
+ * matrix-operand assembly, and writes every cached K and V row it assembled
+ * to k_out / v_out (bf16 [sum_b L_b][n_kv_heads][head_dim], requests in order,
+ * tokens in logical order) instead of computing attention.  The result must
+ * equal a host gather through page_table bit for bit.  Workspace as for
+ * vd_decode_attn with n_q_heads = n_kv_heads.
+ */
+int vd_decode_gather(const void *k_pages, const void *v_pages,
+                     const int32_t *page_table, const int32_t *seq_lens,
+                     void *k_out, void *v_out, int num_seqs, int n_kv_heads,
+                     int head_dim, int page_size, int max_pages_per_seq,
+                     void *workspace, size_t workspace_bytes,
+                     hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VDECODE_H */

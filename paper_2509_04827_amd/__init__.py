@@ -1,0 +1,165 @@
+"""Python binding of libvdecode (paged GQA decode attention on MI355X).
+
+Argument marshalling only: every step of the decode-attention path runs in the
+HIP kernels of ``libvdecode.so``, reached through its C ABI
+(``include/vdecode.h``) with ctypes.  torch is used for device memory and
+streams.  There is no fallback: if the library is not built, every call
+raises.
+
+The functions carry the C names; tensors stand in for pointers and the sizes
+are read from their shapes:
+
+    q          bf16  [num_seqs, n_q_heads, head_dim]           (cuda)
+    k_pages    bf16  [num_pages, page_size, n_kv_heads, head_dim]
+    v_pages    bf16  same shape as k_pages
+    page_table int32 [num_seqs, max_pages_per_seq]
+    seq_lens   int32 [num_seqs]
+    out        bf16 or float32 [num_seqs, n_q_heads, head_dim]  (float32 sets VD_FLAG_OUT_F32)
+    workspace  uint8 [>= vd_decode_workspace_size(...)]
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libvdecode.so")
+
+VD_SUCCESS = 0
+VD_ERROR_INVALID_VALUE = 1
+VD_ERROR_NOT_SUPPORTED = 2
+VD_ERROR_WORKSPACE_TOO_SMALL = 3
+VD_ERROR_LAUNCH = 4
+VD_FLAG_OUT_F32 = 1 << 0
+VD_FLAG_SPLIT_SHIFT = 8
+
+EXPORTS = ("vd_status_string", "vd_decode_workspace_size", "vd_decode_attn", "vd_decode_plan",
+           "vd_decode_partial", "vd_decode_combine", "vd_decode_gather")
+
+
+def VD_FLAG_SPLIT_PAGES(n: int) -> int:
+    return (int(n) & 0xFF) << VD_FLAG_SPLIT_SHIFT
+
+
+class VdError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__("%s returned %d (%s)" % (where, status, vd_status_string(status)))
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libvdecode.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libvdecode.so is not built: run python -m paper_2509_04827_amd.build "
+                               "(or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I, U, Z, F = ctypes.c_void_p, ctypes.c_int, ctypes.c_uint, ctypes.c_size_t, ctypes.c_float
+        L.vd_status_string.argtypes = [I]
+        L.vd_status_string.restype = ctypes.c_char_p
+        L.vd_decode_workspace_size.argtypes = [I, I, I, I, I, I, U]
+        L.vd_decode_workspace_size.restype = Z
+        attn = [P, P, P, P, P, P, I, I, I, I, I, F, I, P, Z, U, P]
+        L.vd_decode_attn.argtypes = attn
+        L.vd_decode_partial.argtypes = attn
+        L.vd_decode_plan.argtypes = [P, I, I, I, I, I, I, P, Z, U, P]
+        L.vd_decode_combine.argtypes = [P, I, I, I, I, I, I, P, Z, U, P]
+        L.vd_decode_gather.argtypes = [P, P, P, P, P, P, I, I, I, I, I, P, Z, P]
+        for n in ("vd_decode_attn", "vd_decode_partial", "vd_decode_plan", "vd_decode_combine",
+                  "vd_decode_gather"):
+            getattr(L, n).restype = I
+        _lib = L
+    return _lib
+
+
+def vd_status_string(status: int) -> str:
+    return lib().vd_status_string(int(status)).decode()
+
+
+def vd_decode_workspace_size(num_seqs: int, n_q_heads: int, n_kv_heads: int, head_dim: int = 128,
+                             page_size: int = 16, max_pages_per_seq: int = 1,
+                             flags: int = 0) -> int:
+    return int(lib().vd_decode_workspace_size(num_seqs, n_q_heads, n_kv_heads, head_dim,
+                                              page_size, max_pages_per_seq, flags))
+
+
+def alloc_workspace(num_seqs, n_q_heads, n_kv_heads, max_pages_per_seq, flags=0,
+                    head_dim=128, page_size=16, device="cuda") -> torch.Tensor:
+    n = vd_decode_workspace_size(num_seqs, n_q_heads, n_kv_heads, head_dim, page_size,
+                                 max_pages_per_seq, flags)
+    if n == 0:
+        raise VdError(VD_ERROR_INVALID_VALUE, "vd_decode_workspace_size")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(st, where):
+    if st != VD_SUCCESS:
+        raise VdError(st, where)
+
+
+def _attn_sizes(q, k_pages, page_table):
+    B, Hq, D = q.shape
+    _, S, Hkv, _ = k_pages.shape
+    return B, Hq, Hkv, D, S, page_table.shape[1]
+
+
+def _out_flags(out, flags):
+    return flags | (VD_FLAG_OUT_F32 if out.dtype == torch.float32 else 0)
+
+
+def vd_decode_attn(q, k_pages, v_pages, page_table, seq_lens, out, scale: float, workspace,
+                   flags: int = 0, stream=None) -> None:
+    B, Hq, Hkv, D, S, maxp = _attn_sizes(q, k_pages, page_table)
+    _check(lib().vd_decode_attn(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(page_table),
+                                _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale), maxp,
+                                _ptr(workspace), workspace.numel(), _out_flags(out, flags),
+                                _stream(stream)), "vd_decode_attn")
+
+
+def vd_decode_plan(seq_lens, n_q_heads: int, n_kv_heads: int, max_pages_per_seq: int, workspace,
+                   flags: int = 0, head_dim: int = 128, page_size: int = 16, stream=None) -> None:
+    _check(lib().vd_decode_plan(_ptr(seq_lens), seq_lens.shape[0], n_q_heads, n_kv_heads,
+                                head_dim, page_size, max_pages_per_seq, _ptr(workspace),
+                                workspace.numel(), flags, _stream(stream)), "vd_decode_plan")
+
+
+def vd_decode_partial(q, k_pages, v_pages, page_table, seq_lens, out, scale: float, workspace,
+                      flags: int = 0, stream=None) -> None:
+    B, Hq, Hkv, D, S, maxp = _attn_sizes(q, k_pages, page_table)
+    _check(lib().vd_decode_partial(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(page_table),
+                                   _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale),
+                                   maxp, _ptr(workspace), workspace.numel(),
+                                   _out_flags(out, flags), _stream(stream)), "vd_decode_partial")
+
+
+def vd_decode_combine(out, n_kv_heads: int, max_pages_per_seq: int, workspace, flags: int = 0,
+                      page_size: int = 16, stream=None) -> None:
+    B, Hq, D = out.shape
+    _check(lib().vd_decode_combine(_ptr(out), B, Hq, n_kv_heads, D, page_size, max_pages_per_seq,
+                                   _ptr(workspace), workspace.numel(), _out_flags(out, flags),
+                                   _stream(stream)), "vd_decode_combine")
+
+
+def vd_decode_gather(k_pages, v_pages, page_table, seq_lens, k_out, v_out, workspace,
+                     stream=None) -> None:
+    _, S, Hkv, D = k_pages.shape
+    _check(lib().vd_decode_gather(_ptr(k_pages), _ptr(v_pages), _ptr(page_table), _ptr(seq_lens),
+                                  _ptr(k_out), _ptr(v_out), seq_lens.shape[0], Hkv, D, S,
+                                  page_table.shape[1], _ptr(workspace), workspace.numel(),
+                                  _stream(stream)), "vd_decode_gather")

@@ -1,0 +1,129 @@
+"""C-ABI library on the CPU: it loads, exports what include/vdecode.h declares,
+sizes workspaces sensibly and rejects bad arguments before touching the GPU.
+No call here reaches a kernel launch (every argument set is invalid)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2509_04827_amd as vd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "vdecode.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(vd_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = vd.lib()
+    names = declared_functions()
+    assert names, "no declarations parsed"
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(vd.EXPORTS)
+
+
+def test_status_strings():
+    assert vd.vd_status_string(0) == "VD_SUCCESS"
+    assert vd.vd_status_string(3) == "VD_ERROR_WORKSPACE_TOO_SMALL"
+    assert vd.vd_status_string(99) == "VD_UNKNOWN_STATUS"
+
+
+def test_workspace_size_rules():
+    ws = vd.vd_decode_workspace_size
+    base = ws(256, 32, 8, 128, 16, 1024)
+    assert base > 0
+    assert ws(256, 32, 8, 128, 16, 1024) == base          # deterministic
+    assert ws(256, 64, 8, 128, 16, 1024) > base            # more heads per group
+    assert ws(0, 32, 8, 128, 16, 1) > 0                    # empty batch is valid
+    assert ws(256, 32, 8, 64, 16, 1024) == 0               # head_dim unsupported
+    assert ws(256, 32, 8, 128, 32, 1024) == 0              # page_size unsupported
+    assert ws(256, 24, 8, 128, 16, 1024) == 0              # G = 3 unsupported
+    assert ws(256, 30, 8, 128, 16, 1024) == 0              # Hq % Hkv != 0
+    assert ws(8193, 32, 8, 128, 16, 16) == 0               # too many requests
+    assert ws(4, 32, 8, 128, 16, 63, 1 << 5) == 0          # unknown flag bit
+    assert ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_SPLIT_PAGES(65)) == 0
+    # forcing one page per split needs one partial per (page, KV head) at most
+    small = ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_SPLIT_PAGES(1))
+    assert small >= 4 * 63 * 8 * 4 * 128 * 4
+
+
+P = ctypes.c_void_p
+FAKE = P(0x10000)      # aligned, never dereferenced: validation fails first
+MIS = P(0x10002)       # misaligned
+
+
+def call_attn(fn, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, pt=FAKE, sl=FAKE, out=FAKE, B=4, Hq=32, Hkv=8, D=128, S=16,
+             scale=0.088, maxp=63, ws=FAKE, wsb=0, flags=0, stream=None)
+    a.update(kw)
+    return fn(a["q"], a["k"], a["v"], a["pt"], a["sl"], a["out"], a["B"], a["Hq"], a["Hkv"],
+              a["D"], a["S"], a["scale"], a["maxp"], a["ws"], a["wsb"], a["flags"], a["stream"])
+
+
+@pytest.mark.parametrize("entry", ["vd_decode_attn", "vd_decode_partial"])
+def test_argument_errors(entry):
+    fn = getattr(vd.lib(), entry)
+    need = vd.vd_decode_workspace_size(4, 32, 8, 128, 16, 63)
+    ok = dict(wsb=need)
+    assert call_attn(fn, q=None, **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, out=None, **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, ws=None, **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, q=MIS, **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, k=MIS, **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, pt=P(0x10001), **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, B=-1, **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, Hq=30, **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, maxp=0, **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, scale=float("nan"), **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, scale=float("inf"), **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, flags=1 << 7, **ok) == vd.VD_ERROR_INVALID_VALUE
+    assert call_attn(fn, D=64, **ok) == vd.VD_ERROR_NOT_SUPPORTED
+    assert call_attn(fn, S=32, **ok) == vd.VD_ERROR_NOT_SUPPORTED
+    assert call_attn(fn, Hq=24, **ok) == vd.VD_ERROR_NOT_SUPPORTED
+    assert call_attn(fn, Hq=256, Hkv=8, **ok) == vd.VD_ERROR_NOT_SUPPORTED   # G = 32
+    assert call_attn(fn, B=9000, **ok) == vd.VD_ERROR_NOT_SUPPORTED
+    assert call_attn(fn, wsb=need - 1) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
+    assert call_attn(fn, wsb=0) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
+    forced = vd.VD_FLAG_SPLIT_PAGES(1)
+    need1 = vd.vd_decode_workspace_size(4, 32, 8, 128, 16, 63, forced)
+    assert call_attn(fn, wsb=need1 - 1, flags=forced) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
+
+
+def test_plan_combine_gather_argument_errors():
+    L = vd.lib()
+    need = vd.vd_decode_workspace_size(4, 32, 8, 128, 16, 63)
+    assert L.vd_decode_plan(None, 4, 32, 8, 128, 16, 63, FAKE, need, 0, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_decode_plan(FAKE, 4, 32, 8, 128, 16, 63, FAKE, need - 1, 0, None) == \
+        vd.VD_ERROR_WORKSPACE_TOO_SMALL
+    assert L.vd_decode_plan(FAKE, 4, 32, 8, 128, 8, 63, FAKE, need, 0, None) == vd.VD_ERROR_NOT_SUPPORTED
+    assert L.vd_decode_combine(None, 4, 32, 8, 128, 16, 63, FAKE, need, 0, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_decode_combine(MIS, 4, 32, 8, 128, 16, 63, FAKE, need, 0, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_decode_combine(FAKE, 4, 32, 8, 128, 16, 63, FAKE, 0, 0, None) == \
+        vd.VD_ERROR_WORKSPACE_TOO_SMALL
+    gneed = vd.vd_decode_workspace_size(4, 8, 8, 128, 16, 63)
+    assert L.vd_decode_gather(FAKE, FAKE, FAKE, FAKE, None, FAKE, 4, 8, 128, 16, 63, FAKE, gneed,
+                              None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_decode_gather(FAKE, FAKE, FAKE, FAKE, FAKE, MIS, 4, 8, 128, 16, 63, FAKE, gneed,
+                              None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_decode_gather(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 8, 128, 16, 63, FAKE,
+                              gneed - 1, None) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
+    assert L.vd_decode_gather(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 8, 96, 16, 63, FAKE, gneed,
+                              None) == vd.VD_ERROR_NOT_SUPPORTED
+
+
+def test_product_does_not_reference_oracle():
+    """The product package neither imports nor links the oracle."""
+    pkg = os.path.join(ROOT, "paper_2509_04827_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in text and "vdo_" not in text, f
+    with open(os.path.join(pkg, "libvdecode.so"), "rb") as fh:
+        blob = fh.read()
+    assert b"vdo_" not in blob and b"libvdo_oracle" not in blob

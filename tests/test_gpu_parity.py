@@ -1,0 +1,305 @@
+"""GPU parity of libvdecode against the fp64 oracle, called through the C ABI.
+
+Gates (fp32 output): max-abs <= 1e-2 and rel-L2 <= 5e-3 over the whole output
+of a workload.  bf16 output adds its own rounding (half an ulp, up to 0.0156
+for |out| in [4, 8)), so its gate is rel-L2 <= 5e-3 and, per element,
+|err| <= max(1e-2, one bf16 ulp of the oracle value).  Copy-through gather,
+L = 1, one-hot, page permutation, NaN fill and determinism are bit-exact.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import oracle_pins as pins
+import paper_2509_04827_amd as vd
+from workloads import ORDER, Workload, bits, make_case
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def dev_case(c):
+    return {k: (c[k].to(DEV) if isinstance(c.get(k), torch.Tensor) else c[k]) for k in c}
+
+
+def host(c):
+    return (bits(c["q"]), bits(c["k_pages"]), bits(c["v_pages"]), c["page_table"].numpy(),
+            c["seq_lens"].numpy())
+
+
+def run_gpu(d, out_dtype=torch.float32, flags=0, ws=None):
+    out = torch.full(d["q"].shape, float("nan"), dtype=out_dtype, device=DEV)
+    if ws is None:
+        ws = vd.alloc_workspace(d["num_seqs"], d["n_q_heads"], d["n_kv_heads"],
+                                d["max_pages_per_seq"], flags)
+    vd.vd_decode_attn(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"], out,
+                      d["scale"], ws, flags=flags)
+    torch.cuda.synchronize()
+    return out
+
+
+def ref_of(c):
+    return oracle.decode_attn(*host(c), c["scale"])
+
+
+def bf16_ulp(x):
+    a = np.abs(x).astype(np.float32)
+    e = np.floor(np.log2(np.maximum(a, np.float32(2.0 ** -126))))
+    return np.ldexp(1.0, (e - 7).astype(np.int64))
+
+
+def check_f32(got, ref, what):
+    got = got.double().cpu().numpy() if isinstance(got, torch.Tensor) else got
+    assert np.isfinite(got).all(), "%s: non-finite output" % what
+    err = np.abs(got - ref)
+    rel = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300)
+    say("%s: fp32 out max-abs %.3e rel-L2 %.3e" % (what, err.max(), rel))
+    assert err.max() <= 1e-2 and rel <= 5e-3, what
+    return err.max(), rel
+
+
+def check_bf16(got, ref, what):
+    got = got.float().cpu().double().numpy()
+    assert np.isfinite(got).all()
+    err = np.abs(got - ref)
+    rel = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300)
+    bound = np.maximum(1e-2, bf16_ulp(ref))
+    say("%s: bf16 out max-abs %.3e rel-L2 %.3e worst err/bound %.3f"
+        % (what, err.max(), rel, (err / bound).max()))
+    assert rel <= 5e-3 and (err <= bound).all(), what
+
+
+def custom(lengths, hq=32, hkv=8, seed=0, fill="nan", shuffle=True, pt_stride=None):
+    w = Workload("custom", len(lengths), hq, hkv, 128, 16, "fixed", tuple(lengths))
+    return make_case(w, seed=seed, fill=fill, shuffle=shuffle, pt_stride=pt_stride)
+
+
+# ------------------------------------------------------------------ workloads
+@pytest.mark.parametrize("name", ORDER)
+def test_workload_parity(name):
+    say("case: workload %s seed 0" % name)
+    c = make_case(name, seed=0, fill="nan")
+    say("  N_req %d N_kv %d pages %d" % (c["num_seqs"], c["n_kv"], c["num_pages"]))
+    d = dev_case(c)
+    got32 = run_gpu(d, torch.float32)
+    got16 = run_gpu(d, torch.bfloat16)
+    ref = ref_of(c)
+    check_f32(got32, ref, name)
+    check_bf16(got16, ref, name)
+
+
+# ------------------------------------------------------------------ bit-exact gather
+@pytest.mark.parametrize("name", ["tiny_b4", "llama8b_b64", "long_b16", "edges"])
+def test_gather_copy_through_bit_exact(name):
+    say("case: gather %s" % name)
+    if name == "edges":
+        c = custom([1, 15, 16, 17, 0, 33, 64, 1000, 3], hkv=8)
+    else:
+        c = make_case(name, seed=0, fill="nan")
+    d = dev_case(c)
+    n = c["n_kv"]
+    ko = torch.empty((max(n, 1), c["n_kv_heads"], 128), dtype=torch.bfloat16, device=DEV)
+    vo = torch.empty_like(ko)
+    ws = vd.alloc_workspace(c["num_seqs"], c["n_kv_heads"], c["n_kv_heads"], c["max_pages_per_seq"])
+    vd.vd_decode_gather(d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"], ko, vo, ws)
+    torch.cuda.synchronize()
+    kr, vr = oracle.gather(bits(c["k_pages"]), bits(c["v_pages"]), c["page_table"].numpy(),
+                           c["seq_lens"].numpy())
+    assert np.array_equal(bits(ko[:n].cpu()), kr)
+    assert np.array_equal(bits(vo[:n].cpu()), vr)
+
+
+# ------------------------------------------------------------------ closed forms, exact
+def test_single_token_is_v_row():
+    say("case: L=1 x 37 requests")
+    c = custom([1] * 37, hq=32, hkv=8, seed=3)
+    d = dev_case(c)
+    pt = c["page_table"].numpy()
+    vrows = bits(c["v_pages"])[pt[:, 0], 0]                    # [B][Hkv][D]
+    expect = np.repeat(vrows, 4, axis=1)                       # [B][Hq][D]
+    got16 = bits(run_gpu(d, torch.bfloat16).cpu())
+    assert np.array_equal(got16, expect)
+    got32 = run_gpu(d, torch.float32).cpu().numpy()
+    assert np.array_equal(got32, (expect.astype(np.uint32) << 16).view(np.float32))
+
+
+@pytest.mark.parametrize("split", [0, 1, 3])
+def test_one_hot_is_v_row(split):
+    lengths = [1, 40, 300, 17, 2000, 5000, 16, 33]
+    hot = [0, 39, 150, 16, 1999, 2500, 0, 32]
+    say("case: one-hot split=%d" % split)
+    c = pins.onehot_case(lengths, 32, 8, 11, hot)
+    q = torch.from_numpy(c["q"].view(np.int16)).view(torch.bfloat16)
+    k = torch.from_numpy(c["k"].view(np.int16)).view(torch.bfloat16)
+    v = torch.from_numpy(c["v"].view(np.int16)).view(torch.bfloat16)
+    d = dict(q=q.to(DEV), k_pages=k.to(DEV), v_pages=v.to(DEV),
+             page_table=torch.from_numpy(c["pt"]).to(DEV), seq_lens=torch.from_numpy(c["L"]).to(DEV),
+             scale=c["scale"], num_seqs=len(lengths), n_q_heads=32, n_kv_heads=8,
+             max_pages_per_seq=c["pt"].shape[1])
+    flags = vd.VD_FLAG_SPLIT_PAGES(split) if split else 0
+    got = run_gpu(d, torch.float32, flags=flags).cpu().numpy()
+    for b, t in enumerate(hot):
+        vrow = c["v"][c["pt"][b, t // 16], t % 16]             # [Hkv][D]
+        expect = (np.repeat(vrow, 4, axis=0).astype(np.uint32) << 16).view(np.float32)
+        assert np.array_equal(got[b], expect), b
+
+
+def test_constant_v():
+    say("case: constant V")
+    c = custom([1, 15, 16, 17, 100, 3000], hq=32, hkv=8, seed=4)
+    vb = c["v_pages"].view(torch.int16)
+    const = torch.randn(8, 128).to(torch.bfloat16).view(torch.int16)
+    pt = c["page_table"].numpy()
+    for b, n in enumerate(c["seq_lens"].tolist()):
+        for t in range(n):
+            vb[pt[b, t // 16], t % 16] = const
+    got = run_gpu(dev_case(c), torch.float32).cpu().double()
+    expect = const.view(torch.bfloat16).double().repeat_interleave(4, dim=0)
+    rel = ((got - expect).abs() / expect.abs().clamp_min(1e-30)).max().item()
+    say("  constant V max rel %.3e" % rel)
+    assert rel <= 1e-5
+
+
+# ------------------------------------------------------------------ invariances
+def test_page_permutation_bit_exact():
+    say("case: page permutation")
+    lengths = [37, 128, 500, 1000, 4000, 1]
+    a = custom(lengths, seed=6, shuffle=False)
+    perm = torch.randperm(a["num_pages"], generator=torch.Generator().manual_seed(9))
+    b = dict(a)
+    b["k_pages"] = torch.empty_like(a["k_pages"])
+    b["v_pages"] = torch.empty_like(a["v_pages"])
+    b["k_pages"][perm] = a["k_pages"]
+    b["v_pages"][perm] = a["v_pages"]
+    b["page_table"] = perm.to(torch.int32)[a["page_table"].long()]
+    for dt in (torch.float32, torch.bfloat16):
+        x = run_gpu(dev_case(a), dt).cpu()
+        y = run_gpu(dev_case(b), dt).cpu()
+        assert torch.equal(x.view(torch.int16) if dt == torch.bfloat16 else x.view(torch.int32),
+                           y.view(torch.int16) if dt == torch.bfloat16 else y.view(torch.int32))
+
+
+def test_nan_fill_and_determinism():
+    say("case: NaN vs zero fill, determinism")
+    lengths = [5, 17, 31, 250, 1111, 4097]
+    a = custom(lengths, seed=7, fill="nan")
+    z = custom(lengths, seed=7, fill="zero")
+    x1 = run_gpu(dev_case(a)).cpu()
+    x2 = run_gpu(dev_case(a)).cpu()
+    y = run_gpu(dev_case(z)).cpu()
+    assert torch.isfinite(x1).all()
+    assert torch.equal(x1.view(torch.int32), x2.view(torch.int32))
+    assert torch.equal(x1.view(torch.int32), y.view(torch.int32))
+
+
+def test_split_invariance():
+    say("case: forced split sizes")
+    c = make_case("tiny_b4", seed=0)
+    extra = custom([3000, 77, 1, 4096, 700], seed=8)
+    for cc in (c, extra):
+        d = dev_case(cc)
+        base = run_gpu(d).cpu().double()
+        ref = ref_of(cc)
+        check_f32(base, ref, "split auto")
+        for s in (1, 2, 7, 64):
+            got = run_gpu(d, flags=vd.VD_FLAG_SPLIT_PAGES(s)).cpu().double()
+            rel = ((got - base).norm() / base.norm()).item()
+            say("  split %d rel diff %.3e" % (s, rel))
+            assert rel <= 1e-5
+            check_f32(got, ref, "split %d" % s)
+
+
+def test_pt_stride():
+    say("case: wide page-table rows")
+    c = custom([100, 7, 900], seed=10, pt_stride=200)
+    check_f32(run_gpu(dev_case(c)), ref_of(c), "pt stride 200")
+
+
+# ------------------------------------------------------------------ shapes and edges
+def test_page_boundary_lengths():
+    lengths = [1, 15, 16, 17, 31, 32, 33, 255, 256, 257, 1023, 1024, 1025]
+    say("case: page-boundary lengths %s" % lengths)
+    c = custom(lengths, seed=12)
+    d = dev_case(c)
+    ref = ref_of(c)
+    check_f32(run_gpu(d), ref, "boundaries")
+    check_bf16(run_gpu(d, torch.bfloat16), ref, "boundaries")
+
+
+@pytest.mark.parametrize("G,hkv", [(1, 4), (2, 4), (4, 2), (8, 2), (16, 1), (8, 8)])
+def test_gqa_ratios(G, hkv):
+    say("case: G=%d Hkv=%d" % (G, hkv))
+    c = custom([1, 20, 300, 2222, 64], hq=G * hkv, hkv=hkv, seed=13 + G)
+    d = dev_case(c)
+    ref = ref_of(c)
+    check_f32(run_gpu(d), ref, "G=%d" % G)
+    check_bf16(run_gpu(d, torch.bfloat16), ref, "G=%d" % G)
+
+
+def test_empty_requests():
+    say("case: empty requests")
+    c = custom([0, 5, 0, 300, 0], seed=14)
+    got = run_gpu(dev_case(c)).cpu()
+    assert torch.equal(got[0], torch.zeros_like(got[0])) and torch.equal(got[2], torch.zeros_like(got[2]))
+    assert torch.equal(got[4], torch.zeros_like(got[4]))
+    check_f32(got, ref_of(c), "empty")
+    z = custom([0, 0, 0], seed=15)
+    got = run_gpu(dev_case(z)).cpu()
+    assert torch.equal(got, torch.zeros_like(got))
+
+
+def test_large_scores():
+    """Scores around 5.8e3: only a max-subtracted softmax survives."""
+    say("case: large scores")
+    c = custom([40, 3, 777, 5000], seed=16, fill="zero")
+    c["k_pages"].view(torch.int16)[:, :, :, 7] = pins.bf16_bits(256.0)
+    c["q"].view(torch.int16)[:, :, 7] = pins.bf16_bits(256.0)
+    check_f32(run_gpu(dev_case(c)), ref_of(c), "large scores")
+
+
+def test_staged_plan_once_two_layers():
+    say("case: plan once, two attention layers")
+    c = custom([33, 900, 5000, 1], seed=17)
+    c2 = custom([33, 900, 5000, 1], seed=18, fill="zero")
+    d, d2 = dev_case(c), dev_case(c2)
+    ws = vd.alloc_workspace(4, 32, 8, c["max_pages_per_seq"])
+    vd.vd_decode_plan(d["seq_lens"], 32, 8, c["max_pages_per_seq"], ws)
+    outs = []
+    for dd in (d, d2):
+        out = torch.empty(dd["q"].shape, dtype=torch.float32, device=DEV)
+        # same lengths and placement; different values (another layer)
+        vd.vd_decode_partial(dd["q"], dd["k_pages"], dd["v_pages"], d["page_table"],
+                             d["seq_lens"], out, dd["scale"], ws)
+        vd.vd_decode_combine(out, 8, c["max_pages_per_seq"], ws)
+        outs.append(out)
+    torch.cuda.synchronize()
+    c2["page_table"] = c["page_table"]
+    check_f32(outs[0], ref_of(c), "layer 0")
+    check_f32(outs[1], ref_of(c2), "layer 1")
+    fused = run_gpu(d)
+    assert torch.equal(outs[0].view(torch.int32).cpu(), fused.view(torch.int32).cpu())
+
+
+def test_device_errors_leave_stream_clean():
+    say("case: error codes on device")
+    c = custom([10], seed=19)
+    d = dev_case(c)
+    out = torch.empty(d["q"].shape, dtype=torch.float32, device=DEV)
+    small = torch.empty(16, dtype=torch.uint8, device=DEV)
+    with pytest.raises(vd.VdError) as e:
+        vd.vd_decode_attn(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"], out,
+                          d["scale"], small)
+    assert e.value.status == vd.VD_ERROR_WORKSPACE_TOO_SMALL
+    with pytest.raises(vd.VdError) as e:
+        vd.vd_decode_attn(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"], out,
+                          math.nan, small)
+    assert e.value.status == vd.VD_ERROR_INVALID_VALUE
+    check_f32(run_gpu(d), ref_of(c), "after errors")
