@@ -64,23 +64,25 @@ typedef enum vd_status {
 
 /* flags */
 #define VD_FLAG_OUT_F32 (1u << 0)     /* out is fp32 instead of bf16 */
-/* bits 8..15: force the split size to this many pages (1..64); 0 = automatic.
- * For tests of split invariance; the workspace must hold the resulting plan. */
-#define VD_FLAG_SPLIT_SHIFT 8u
-#define VD_FLAG_SPLIT_MASK (0xFFu << VD_FLAG_SPLIT_SHIFT)
-#define VD_FLAG_SPLIT_PAGES(n) (((unsigned)(n) & 0xFFu) << VD_FLAG_SPLIT_SHIFT)
+/* bits 8..15: cut the step's (page, KV head) tiles into ranges of this many
+ * tiles (1..255) instead of the automatic partition (0).  Changes where the
+ * split-K boundaries fall, not the result beyond rounding; for tests.  The
+ * workspace must be sized with the same flags. */
+#define VD_FLAG_RANGE_SHIFT 8u
+#define VD_FLAG_RANGE_MASK (0xFFu << VD_FLAG_RANGE_SHIFT)
+#define VD_FLAG_RANGE_TILES(n) (((unsigned)(n) & 0xFFu) << VD_FLAG_RANGE_SHIFT)
 
 /* Human-readable name of a vd_status value; never NULL. */
 const char *vd_status_string(int status);
 
 /*
- * Bytes of device workspace a call with these sizes needs: the split plan and
- * the split partials (per split and query head: running max, normaliser and an
- * fp32 head_dim accumulator).  Independent of the actual lengths; grows with
- * num_seqs * max_pages_per_seq only for very large caches.  `flags` as passed
- * to the attention call: a forced split size (VD_FLAG_SPLIT_PAGES) can need
- * more room than the automatic plan.  Returns 0 when the sizes or flags are
- * invalid or unsupported.
+ * Bytes of device workspace a call with these sizes needs: the plan and the
+ * split-K partials (per partial and query head: running max, normaliser and
+ * an fp32 head_dim accumulator).  Independent of the actual lengths; grows
+ * with num_seqs * max_pages_per_seq * n_kv_heads / 256 for very large caches.
+ * `flags` as passed to the attention call: a forced range length
+ * (VD_FLAG_RANGE_TILES) can need more room than the automatic plan.  Returns
+ * 0 when the sizes or flags are invalid or unsupported.
  */
 size_t vd_decode_workspace_size(int num_seqs, int n_q_heads, int n_kv_heads,
                                 int head_dim, int page_size,
@@ -100,10 +102,11 @@ int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
                    size_t workspace_bytes, unsigned flags, hipStream_t stream);
 
 /*
- * Stage 1 of 3: split every request's page range into load-balanced chunks
- * (one work item per chunk and KV head) and write the plan into the
- * workspace.  Depends only on seq_lens and the sizes, so one plan serves
- * every layer of a decode step.
+ * Stage 1 of 3: lay every (page, KV head) tile of the step out in one sequence
+ * (request, KV head, page order) and cut it into as many equal ranges as the
+ * device runs waves at once, so every wave streams the same number of tiles
+ * whatever the length mix; write that plan into the workspace.  Depends only
+ * on seq_lens and the sizes, so one plan serves every layer of a decode step.
  */
 int vd_decode_plan(const int32_t *seq_lens, int num_seqs, int n_q_heads,
                    int n_kv_heads, int head_dim, int page_size,
@@ -111,10 +114,12 @@ int vd_decode_plan(const int32_t *seq_lens, int num_seqs, int n_q_heads,
                    size_t workspace_bytes, unsigned flags, hipStream_t stream);
 
 /*
- * Stage 2 of 3: attention over every work item of the plan in `workspace`.
- * Requests that fit in one chunk get their final output here; the others
- * leave per-chunk partials in the workspace.  Arguments as vd_decode_attn;
- * seq_lens, the sizes and flags must match the plan's.
+ * Stage 2 of 3: attention over every range of the plan in `workspace`.  A
+ * (request, KV head) whose tiles fall in one range gets its final output
+ * here; the others leave one partial per range they touch in the workspace.
+ * Arguments as vd_decode_attn; seq_lens, the sizes and flags must match the
+ * plan's.  Several calls may follow one plan (one per layer), each finished
+ * by vd_decode_combine before the next reuses the workspace.
  */
 int vd_decode_partial(const void *q, const void *k_pages, const void *v_pages,
                       const int32_t *page_table, const int32_t *seq_lens,

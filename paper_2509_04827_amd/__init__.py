@@ -33,14 +33,14 @@ VD_ERROR_NOT_SUPPORTED = 2
 VD_ERROR_WORKSPACE_TOO_SMALL = 3
 VD_ERROR_LAUNCH = 4
 VD_FLAG_OUT_F32 = 1 << 0
-VD_FLAG_SPLIT_SHIFT = 8
+VD_FLAG_RANGE_SHIFT = 8
 
 EXPORTS = ("vd_status_string", "vd_decode_workspace_size", "vd_decode_attn", "vd_decode_plan",
            "vd_decode_partial", "vd_decode_combine", "vd_decode_gather")
 
 
-def VD_FLAG_SPLIT_PAGES(n: int) -> int:
-    return (int(n) & 0xFF) << VD_FLAG_SPLIT_SHIFT
+def VD_FLAG_RANGE_TILES(n: int) -> int:
+    return (int(n) & 0xFF) << VD_FLAG_RANGE_SHIFT
 
 
 class VdError(RuntimeError):

@@ -46,10 +46,10 @@ def test_workspace_size_rules():
     assert ws(256, 30, 8, 128, 16, 1024) == 0              # Hq % Hkv != 0
     assert ws(8193, 32, 8, 128, 16, 16) == 0               # too many requests
     assert ws(4, 32, 8, 128, 16, 63, 1 << 5) == 0          # unknown flag bit
-    assert ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_SPLIT_PAGES(65)) == 0
-    # forcing one page per split needs one partial per (page, KV head) at most
-    small = ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_SPLIT_PAGES(1))
-    assert small >= 4 * 63 * 8 * 4 * 128 * 4
+    # one tile per range: up to one partial per (page, KV head) plus one per segment
+    small = ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_RANGE_TILES(1))
+    assert small >= (4 * 63 * 8 + 4 * 8) * 4 * 128 * 4
+    assert ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_RANGE_TILES(200)) < small
 
 
 P = ctypes.c_void_p
@@ -89,7 +89,7 @@ def test_argument_errors(entry):
     assert call_attn(fn, B=9000, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     assert call_attn(fn, wsb=need - 1) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
     assert call_attn(fn, wsb=0) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
-    forced = vd.VD_FLAG_SPLIT_PAGES(1)
+    forced = vd.VD_FLAG_RANGE_TILES(1)
     need1 = vd.vd_decode_workspace_size(4, 32, 8, 128, 16, 63, forced)
     assert call_attn(fn, wsb=need1 - 1, flags=forced) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
 

@@ -144,7 +144,7 @@ def test_one_hot_is_v_row(split):
              page_table=torch.from_numpy(c["pt"]).to(DEV), seq_lens=torch.from_numpy(c["L"]).to(DEV),
              scale=c["scale"], num_seqs=len(lengths), n_q_heads=32, n_kv_heads=8,
              max_pages_per_seq=c["pt"].shape[1])
-    flags = vd.VD_FLAG_SPLIT_PAGES(split) if split else 0
+    flags = vd.VD_FLAG_RANGE_TILES(split) if split else 0
     got = run_gpu(d, torch.float32, flags=flags).cpu().numpy()
     for b, t in enumerate(hot):
         vrow = c["v"][c["pt"][b, t // 16], t % 16]             # [Hkv][D]
@@ -201,7 +201,7 @@ def test_nan_fill_and_determinism():
 
 
 def test_split_invariance():
-    say("case: forced split sizes")
+    say("case: forced range lengths")
     c = make_case("tiny_b4", seed=0)
     extra = custom([3000, 77, 1, 4096, 700], seed=8)
     for cc in (c, extra):
@@ -209,8 +209,8 @@ def test_split_invariance():
         base = run_gpu(d).cpu().double()
         ref = ref_of(cc)
         check_f32(base, ref, "split auto")
-        for s in (1, 2, 7, 64):
-            got = run_gpu(d, flags=vd.VD_FLAG_SPLIT_PAGES(s)).cpu().double()
+        for s in (1, 2, 7, 64, 255):
+            got = run_gpu(d, flags=vd.VD_FLAG_RANGE_TILES(s)).cpu().double()
             rel = ((got - base).norm() / base.norm()).item()
             say("  split %d rel diff %.3e" % (s, rel))
             assert rel <= 1e-5
