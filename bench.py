@@ -62,6 +62,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="stop repeating the oracle after this much wall time")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="after timing, copy a BYTES-sized buffer 3 times (a plain copy "
+                         "kernel of known size, to scale HBM counters by)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -125,6 +128,15 @@ def main():
     ms_step = ms_total / K
     attn_ms = [a0[i].elapsed_time(a1[i]) for i in range(K)]
     attn_avg_ms = float(np.mean(attn_ms))
+
+    if args.copy_calibration:
+        n = args.copy_calibration // 4
+        src = torch.ones(n, dtype=torch.int32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     kvb = kv_bytes(c)
     P = (c["seq_lens"].numpy().astype(np.int64) + 15) // 16

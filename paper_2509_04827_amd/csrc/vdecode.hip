@@ -6,22 +6,28 @@
 // cache (Sec. 2.1).  The step is read-bound: every cached K and V byte is read
 // once, so the kernels below are built around HBM traffic, not arithmetic.
 //
-// Work decomposition.  A "tile" is one 16-token page of one KV head: 4 KiB of
-// K and 4 KiB of V.  All tiles of the step are laid out in one sequence,
-// ordered by (request b, KV head g, page j); a "segment" is the run of tiles
-// of one (b, g).  The planner cuts the sequence into W ranges of equal length
-// (W a multiple of the number of resident waves), so every wave streams the
-// same number of tiles whatever the length mix.  A range may end inside a
-// segment and may span several; each (range, segment) overlap is a "piece".
-// A piece that covers its whole segment writes the final output, the others
-// write a (max, normaliser, accumulator) partial that the combine kernel
-// merges.  Pieces form a monotone path in (range, segment), so
-// slot = range + segment numbers them without collisions.
+// Work decomposition.  The KV heads are taken in groups of HW (HW divides
+// n_kv_heads; 4 when it can be): one workgroup of HW waves, one wave per head,
+// walks the pages of a head group together, so the group reads each token's
+// HW head rows (HW x 256 B, contiguous in the token-major page) at about the
+// same time.  A "tile" is one 16-token page of one head group.  All tiles of
+// the step are laid out in one sequence, ordered by (request b, head group
+// q, page j); a "segment" is the run of tiles of one (b, q).  The planner
+// cuts the sequence into W ranges of equal length (W a multiple of the
+// number of resident workgroups), so every workgroup streams the same number
+// of tiles whatever the length mix.  A range may end inside a segment and
+// may span several; each (range, segment) overlap is a "piece".  A piece that
+// covers its whole segment writes the final output, the others write a (max,
+// normaliser, accumulator) partial per head that the combine kernel merges.
+// Pieces form a monotone path in (range, segment), so range + segment numbers
+// them without collisions; a head's partial slot is that times HW plus its
+// index in the group.
 //
 // Three kernels on the caller's stream:
 //   plan_kernel     one workgroup: tile offsets per request, range starts,
 //                   per-segment partial slots.
-//   attn_kernel     one wave per range (grid-stride over ranges).  Per tile:
+//   attn_kernel     one workgroup per range (grid-stride over ranges), one
+//                   wave per KV head of the group.  Per page:
 //                     K rows are loaded straight into MFMA A operands (lane =
 //                     token row); scores = K Q^T with v_mfma_f32_16x16x32_bf16
 //                     against the group's G query heads (zero-padded to 16
@@ -52,9 +58,13 @@ constexpr int kPage = 16;
 constexpr int kMaxSeqs = 8192;         // planner keeps tile offsets in LDS
 constexpr int kMaxRangeTiles = 256;    // four 64-entry page-id windows per piece
 constexpr int kMinRangeTiles = 4;      // small steps: at least this many tiles per range
-constexpr int kMaxResidentWaves = 16384;
+constexpr int kMaxResidentGroups = 4096;
 constexpr int kPlanThreads = 1024;
-constexpr int kAttnThreads = 256;      // 4 independent waves per workgroup
+constexpr int kHeadsPerGroup = 4;      // preferred KV heads (waves) per attention workgroup
+constexpr int kAttnGroupsPerCU = 1;    // resident attention workgroups per CU
+constexpr int kPrefetch = 2;           // pages in flight per wave (ring of page tiles)
+constexpr int kMaxHeadsPerGroup = 8;
+constexpr int kAttnMaxThreads = 64 * kMaxHeadsPerGroup;
 constexpr int kCombineThreads = 64;
 constexpr float kLog2e = 1.4426950408889634f;
 // Lazy rescaling: the running max is only raised when a new score exceeds it
@@ -84,22 +94,34 @@ __host__ __device__ inline long long ceil_div_ll(long long a, long long b) { ret
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
+// KV heads per attention workgroup: the preferred count if it divides Hkv,
+// else the largest power of two that does.
+inline int heads_per_group(int Hkv)
+{
+    for (int hw = kHeadsPerGroup; hw > 1; hw >>= 1)
+        if (Hkv % hw == 0)
+            return hw;
+    return 1;
+}
+
 // Range capacity.  Automatic plans: W = R * ceil(T / (kMaxRangeTiles * R))
-// with R <= kMaxResidentWaves resident waves, so W < R + T / kMaxRangeTiles.
-// A forced range length c: W = ceil(T / c).  T <= B * maxp * Hkv.
+// with R <= kMaxResidentGroups resident workgroups, so W < R + T /
+// kMaxRangeTiles.  A forced range length c: W = ceil(T / c).
+// T <= B * maxp * Hkv / HW tiles; partial slots (W + B * Hkv / HW) * HW.
 inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced)
 {
-    const long long tiles = (long long)B * maxp * Hkv;
+    const int HW = heads_per_group(Hkv);
+    const long long tiles = (long long)B * maxp * (Hkv / HW);
     long long cap = forced > 0 ? ceil_div_ll(tiles, forced)
-                               : kMaxResidentWaves + ceil_div_ll(tiles, kMaxRangeTiles);
+                               : kMaxResidentGroups + ceil_div_ll(tiles, kMaxRangeTiles);
     cap = std::max(cap, 1LL);
-    const long long slots = cap + (long long)B * Hkv;
+    const long long slots = cap * HW + (long long)B * Hkv;
     WsLayout l;
     size_t o = 0;
     l.hdr = o;       o = align_up(o + sizeof(PlanHeader), 256);
     l.tile_base = o; o = align_up(o + sizeof(int) * (size_t)(B + 1), 256);
     l.tok_base = o;  o = align_up(o + sizeof(long long) * (size_t)(B + 1), 256);
-    l.seg = o;       o = align_up(o + sizeof(int2) * (size_t)B * Hkv, 256);
+    l.seg = o;       o = align_up(o + sizeof(int2) * (size_t)B * (Hkv / HW), 256);
     l.ranges = o;    o = align_up(o + sizeof(int4) * (size_t)(cap + 1), 256);
     l.part_ml = o;   o = align_up(o + sizeof(float2) * (size_t)slots * G, 256);
     l.part_acc = o;  o = align_up(o + sizeof(float) * (size_t)slots * G * kHeadDim, 256);
@@ -142,8 +164,8 @@ __device__ inline int range_of(long long t, long long T, long long W)
 }
 
 __global__ void __launch_bounds__(kPlanThreads)
-plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hkv, int maxp, int forced,
-            int resident_waves, char *__restrict__ ws, WsLayout lay)
+plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int forced,
+            int resident_groups, char *__restrict__ ws, WsLayout lay)
 {
     __shared__ int s_pre[kMaxSeqs + 1];
     __shared__ long long s_scan[kPlanThreads];
@@ -157,7 +179,7 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hkv, int maxp, int 
     for (int b0 = 0; b0 < B; b0 += kPlanThreads) {
         const int b = b0 + t;
         const int L = b < B ? clamped_len(seq_lens, b, maxp) : 0;
-        const int tiles = (L + kPage - 1) / kPage * Hkv;
+        const int tiles = (L + kPage - 1) / kPage * Hg;
         long long tot_s, tot_t;
         const long long ex_s = block_exclusive_scan<long long>(tiles, s_scan, tot_s);
         const long long ex_t = block_exclusive_scan<long long>(L, s_scan, tot_t);
@@ -180,7 +202,7 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hkv, int maxp, int 
         } else if (forced > 0) {
             W = ceil_div_ll(T, forced);
         } else {
-            const long long R = resident_waves;
+            const long long R = resident_groups;
             W = std::min<long long>(R, ceil_div_ll(T, kMinRangeTiles));
             if (W == R)
                 W = R * ceil_div_ll(T, (long long)kMaxRangeTiles * R);
@@ -193,7 +215,7 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hkv, int maxp, int 
     __syncthreads();
     const int W = s_W;
 
-    // range starts {b, g, j, t}; range W is the end sentinel
+    // range starts {b, q, j, t}; range W is the end sentinel
     int4 *ranges = (int4 *)(ws + lay.ranges);
     for (int w = t; w <= W; w += kPlanThreads) {
         const long long tt = W ? (long long)w * T / W : 0;
@@ -206,21 +228,21 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hkv, int maxp, int 
             const int mid = (lo + hi) >> 1;
             if (s_pre[mid] <= tt) lo = mid; else hi = mid;
         }
-        const int P = (s_pre[lo + 1] - s_pre[lo]) / Hkv;
+        const int P = (s_pre[lo + 1] - s_pre[lo]) / Hg;
         const int off = (int)(tt - s_pre[lo]);
         ranges[w] = make_int4(lo, off / P, off % P, (int)tt);
     }
 
     // per segment: first partial slot and number of pieces
     int2 *seg = (int2 *)(ws + lay.seg);
-    for (int s = t; s < B * Hkv; s += kPlanThreads) {
-        const int b = s / Hkv, g = s - (s / Hkv) * Hkv;
-        const int P = (s_pre[b + 1] - s_pre[b]) / Hkv;
+    for (int s = t; s < B * Hg; s += kPlanThreads) {
+        const int b = s / Hg, q = s - (s / Hg) * Hg;
+        const int P = (s_pre[b + 1] - s_pre[b]) / Hg;
         if (P == 0) {
             seg[s] = make_int2(0, 0);
             continue;
         }
-        const long long t0 = s_pre[b] + (long long)g * P, t1 = t0 + P - 1;
+        const long long t0 = s_pre[b] + (long long)q * P, t1 = t0 + P - 1;
         const int w0 = range_of(t0, T, W), w1 = range_of(t1, T, W);
         seg[s] = make_int2(w0 + s, w1 - w0 + 1);
     }
@@ -236,7 +258,7 @@ struct AttnArgs {
     const long long *tok_base;
     float2 *part_ml;
     float *part_acc;
-    int Hq, Hkv, pt_stride, maxp;
+    int Hq, Hkv, HW, pt_stride, maxp;
     float scale_log2;
 };
 
@@ -458,30 +480,34 @@ __device__ inline void attn_piece(const AttnArgs &a, int b, int g, int jb, int j
             }
         };
 
-        // Double-buffered page loop with a fixed trip count: the next page's
-        // loads are issued before the current page is consumed (the
-        // scheduling barriers keep the compiler from sinking them).  The last
-        // prefetch of an even page count re-reads the final page, which the
-        // caches serve; every path issues the same loads, so the wait counts
-        // stay exact.
+        // Page loop over a ring of kPrefetch tiles with a fixed trip count: the
+        // loads of page j + kPrefetch - 1 are issued before page j is consumed
+        // (the scheduling barriers keep the compiler from sinking them).
+        // Prefetches past the end re-read the final page, which the caches
+        // serve; every path issues the same loads, so the wait counts stay
+        // exact.
         auto load_page = [&](Tile &T, int jn) {
-            const int pg = ids.get(jn - jb);
+            const int pg = ids.get(min(jn, je - 1) - jb);
             load_tile(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems, koff, voff, row);
         };
-        Tile A, B;
-        load_page(A, jb);
+        Tile ring[kPrefetch];
+#pragma unroll
+        for (int u = 0; u < kPrefetch - 1; ++u)
+            load_page(ring[u], jb + u);
         int j = jb;
-        for (int it = np >> 1; it > 0; --it) {
-            load_page(B, j + 1);
-            __builtin_amdgcn_sched_barrier(0);
-            page_step(A, j);
-            load_page(A, min(j + 2, je - 1));
-            __builtin_amdgcn_sched_barrier(0);
-            page_step(B, j + 1);
-            j += 2;
+        for (int it = np / kPrefetch; it > 0; --it) {
+#pragma unroll
+            for (int u = 0; u < kPrefetch; ++u) {
+                load_page(ring[(u + kPrefetch - 1) % kPrefetch], j + u + kPrefetch - 1);
+                __builtin_amdgcn_sched_barrier(0);
+                page_step(ring[u], j + u);
+            }
+            j += kPrefetch;
         }
-        if (np & 1)
-            page_step(A, j);
+#pragma unroll
+        for (int u = 0; u < kPrefetch - 1; ++u)
+            if (u < np - (j - jb))
+                page_step(ring[u], j + u);
 
         const float l_tot = sum_groups(l_run);
         // acc[blk][i] = O[head r][d 32grp + 8i + blk]
@@ -535,18 +561,17 @@ __device__ inline void attn_piece(const AttnArgs &a, int b, int g, int jb, int j
 }
 
 template <int G, int MODE>
-__global__ void __launch_bounds__(kAttnThreads)
+__global__ void __launch_bounds__(kAttnMaxThreads)
 attn_kernel(const AttnArgs a)
 {
     const int lane = threadIdx.x & 63;
+    const int hi = threadIdx.x >> 6;          // head within the group
     const int W = a.hdr->n_ranges;
-    const int n_waves = gridDim.x * (kAttnThreads / 64);
-    const int Hkv = a.Hkv;
-    for (int w = __builtin_amdgcn_readfirstlane(blockIdx.x * (kAttnThreads / 64) + (threadIdx.x >> 6));
-         w < W; w += n_waves) {
+    const int HW = a.HW, Hg = a.Hkv / a.HW;
+    for (int w = blockIdx.x; w < W; w += gridDim.x) {
         const int4 rs = a.ranges[w];
         const int t_end = a.ranges[w + 1].w;
-        int b = rs.x, g = rs.y, j = rs.z, t = rs.w;
+        int b = rs.x, q = rs.y, j = rs.z, t = rs.w;
         while (t < t_end) {
             const int L = min(a.seq_lens[b], a.maxp * kPage);
             const int P = L > 0 ? (L + kPage - 1) / kPage : 0;
@@ -555,12 +580,13 @@ attn_kernel(const AttnArgs a)
                 continue;
             }
             const int n = min(P - j, t_end - t);
-            const long long segment = (long long)b * Hkv + g;
-            attn_piece<G, MODE>(a, b, g, j, j + n, L, j == 0 && n == P, w + segment, lane);
+            const long long segment = (long long)b * Hg + q;
+            attn_piece<G, MODE>(a, b, q * HW + hi, j, j + n, L, j == 0 && n == P,
+                                (w + segment) * HW + hi, lane);
             t += n;
             j = 0;
-            if (++g == Hkv) {
-                g = 0;
+            if (++q == Hg) {
+                q = 0;
                 ++b;
             }
         }
@@ -573,7 +599,7 @@ struct CombineArgs {
     const int2 *seg;
     const float2 *part_ml;
     const float *part_acc;
-    int Hq, Hkv, G;
+    int Hq, Hkv, G, HW;
 };
 
 template <int MODE>
@@ -583,7 +609,8 @@ combine_kernel(const CombineArgs a)
     const int bh = blockIdx.x;
     const int b = bh / a.Hq, h = bh - (bh / a.Hq) * a.Hq;
     const int g = h / a.G, hh = h - g * a.G;
-    const int2 sg = a.seg[(size_t)b * a.Hkv + g];
+    const int q = g / a.HW, hi = g - q * a.HW;
+    const int2 sg = a.seg[(size_t)b * (a.Hkv / a.HW) + q];
     const int first = sg.x, n = sg.y;
     if (n == 1)
         return;   // the only piece wrote the output
@@ -592,7 +619,7 @@ combine_kernel(const CombineArgs a)
     if (n > 1) {
         float M = -INFINITY;
         for (int s = lane; s < n; s += 64)
-            M = fmaxf(M, a.part_ml[(size_t)(first + s) * a.G + hh].x);
+            M = fmaxf(M, a.part_ml[((size_t)(first + s) * a.HW + hi) * a.G + hh].x);
 #pragma unroll
         for (int off = 32; off >= 1; off >>= 1)
             M = fmaxf(M, __shfl_xor(M, off));
@@ -603,7 +630,7 @@ combine_kernel(const CombineArgs a)
             float2 v[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                const size_t it = (size_t)(first + s + u) * a.G + hh;
+                const size_t it = ((size_t)(first + s + u) * a.HW + hi) * a.G + hh;
                 ml[u] = a.part_ml[it];
                 v[u] = *(const float2 *)(a.part_acc + it * kHeadDim + 2 * lane);
             }
@@ -616,7 +643,7 @@ combine_kernel(const CombineArgs a)
             }
         }
         for (; s < n; ++s) {
-            const size_t it = (size_t)(first + s) * a.G + hh;
+            const size_t it = ((size_t)(first + s) * a.HW + hi) * a.G + hh;
             const float2 ml = a.part_ml[it];
             const float2 v = *(const float2 *)(a.part_acc + it * kHeadDim + 2 * lane);
             const float w = __builtin_amdgcn_exp2f(ml.x - M);
@@ -700,8 +727,9 @@ const void *attn_kernel_ptr(int G, int mode)
 #undef VD_K
 }
 
-// Workgroups of the attention kernel that fit on the device at once.
-int resident_attn_groups(int G, int mode, int *groups)
+// Workgroups of the attention kernel (HW waves each) that fit on the device
+// at once.
+int resident_attn_groups(int G, int mode, int HW, int *groups)
 {
     int cus = 0;
     int st = num_cus(&cus);
@@ -711,10 +739,10 @@ int resident_attn_groups(int G, int mode, int *groups)
     if (!k)
         return VD_ERROR_NOT_SUPPORTED;
     int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, kAttnThreads, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 64 * HW, 0) != hipSuccess ||
         per_cu <= 0)
         return VD_ERROR_LAUNCH;
-    *groups = std::min(cus * per_cu, kMaxResidentWaves / (kAttnThreads / 64));
+    *groups = std::min(cus * std::min(per_cu, kAttnGroupsPerCU), kMaxResidentGroups);
     return VD_SUCCESS;
 }
 
@@ -722,27 +750,28 @@ int enqueue_plan(const int32_t *seq_lens, int num_seqs, int G, int n_kv_heads,
                  int max_pages_per_seq, void *workspace, unsigned flags, int mode,
                  hipStream_t stream)
 {
+    const int HW = heads_per_group(n_kv_heads);
     int groups = 0;
-    int st = resident_attn_groups(G, mode, &groups);
+    int st = resident_attn_groups(G, mode, HW, &groups);
     if (st)
         return st;
     const WsLayout lay = ws_layout(num_seqs, G, n_kv_heads, max_pages_per_seq, forced_tiles(flags));
     hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, seq_lens, num_seqs,
-                       n_kv_heads, max_pages_per_seq, forced_tiles(flags),
-                       groups * (kAttnThreads / 64), (char *)workspace, lay);
+                       n_kv_heads / HW, max_pages_per_seq, forced_tiles(flags), groups,
+                       (char *)workspace, lay);
     return launch_status();
 }
 
 int enqueue_attn(const AttnArgs &args, int G, int mode, hipStream_t stream)
 {
     int groups = 0;
-    int st = resident_attn_groups(G, mode, &groups);
+    int st = resident_attn_groups(G, mode, args.HW, &groups);
     if (st)
         return st;
     const void *k = attn_kernel_ptr(G, mode);
     AttnArgs copy = args;
     void *params[] = {(void *)&copy};
-    if (hipLaunchKernel(k, dim3(groups), dim3(kAttnThreads), params, 0, stream) != hipSuccess)
+    if (hipLaunchKernel(k, dim3(groups), dim3(64 * args.HW), params, 0, stream) != hipSuccess)
         return VD_ERROR_LAUNCH;
     return launch_status();
 }
@@ -759,6 +788,7 @@ AttnArgs make_args(const WsLayout &lay, void *workspace, int n_q_heads, int n_kv
     a.part_acc = (float *)(ws + lay.part_acc);
     a.Hq = n_q_heads;
     a.Hkv = n_kv_heads;
+    a.HW = heads_per_group(n_kv_heads);
     a.pt_stride = max_pages_per_seq;
     a.maxp = max_pages_per_seq;
     a.scale_log2 = scale * kLog2e;
@@ -888,6 +918,7 @@ int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, in
     c.Hq = n_q_heads;
     c.Hkv = n_kv_heads;
     c.G = G;
+    c.HW = heads_per_group(n_kv_heads);
     const dim3 grid((unsigned)num_seqs * n_q_heads);
     if (flags & VD_FLAG_OUT_F32)
         hipLaunchKernelGGL(combine_kernel<MODE_F32>, grid, dim3(kCombineThreads), 0, stream, c);
