@@ -65,7 +65,8 @@ constexpr int kAttnGroupsPerCU = 1;    // resident attention workgroups per CU
 constexpr int kPrefetch = 2;           // pages in flight per wave (ring of page tiles)
 constexpr int kMaxHeadsPerGroup = 8;
 constexpr int kAttnMaxThreads = 64 * kMaxHeadsPerGroup;
-constexpr int kCombineThreads = 64;
+constexpr int kCombineThreads = 256;
+constexpr int kCombineGroupsPerCU = 2;
 constexpr float kLog2e = 1.4426950408889634f;
 // Lazy rescaling: the running max is only raised when a new score exceeds it
 // by more than this (log2 units), so weights stay below 2^8 and acc/l never
@@ -81,12 +82,13 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 struct PlanHeader {
     int n_ranges;  // W
     int n_tiles;   // T
-    int pad[6];
+    int n_merge;   // entries of the merge list
+    int pad[5];
 };
 
 // ---------------------------------------------------------------- workspace
 struct WsLayout {
-    size_t hdr, tile_base, tok_base, seg, ranges, part_ml, part_acc, total;
+    size_t hdr, tok_base, seg, merge, ranges, part_ml, part_acc, total;
     long long cap_ranges, cap_slots;
 };
 
@@ -119,9 +121,9 @@ inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced)
     WsLayout l;
     size_t o = 0;
     l.hdr = o;       o = align_up(o + sizeof(PlanHeader), 256);
-    l.tile_base = o; o = align_up(o + sizeof(int) * (size_t)(B + 1), 256);
     l.tok_base = o;  o = align_up(o + sizeof(long long) * (size_t)(B + 1), 256);
     l.seg = o;       o = align_up(o + sizeof(int2) * (size_t)B * (Hkv / HW), 256);
+    l.merge = o;     o = align_up(o + sizeof(int4) * (size_t)B * (Hkv / HW), 256);
     l.ranges = o;    o = align_up(o + sizeof(int4) * (size_t)(cap + 1), 256);
     l.part_ml = o;   o = align_up(o + sizeof(float2) * (size_t)slots * G, 256);
     l.part_acc = o;  o = align_up(o + sizeof(float) * (size_t)slots * G * kHeadDim, 256);
@@ -132,24 +134,7 @@ inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced)
 }
 
 // ---------------------------------------------------------------- planner
-template <typename T>
-__device__ T block_exclusive_scan(T v, T *sh, T &total)
-{
-    // Hillis-Steele inclusive scan over kPlanThreads values in LDS.
-    const int t = threadIdx.x;
-    sh[t] = v;
-    __syncthreads();
-    for (int off = 1; off < kPlanThreads; off <<= 1) {
-        T add = t >= off ? sh[t - off] : T(0);
-        __syncthreads();
-        sh[t] += add;
-        __syncthreads();
-    }
-    const T incl = sh[t];
-    total = sh[kPlanThreads - 1];
-    __syncthreads();
-    return incl - v;
-}
+constexpr int kPlanPerThread = kMaxSeqs / kPlanThreads;   // requests per planner thread
 
 __device__ inline int clamped_len(const int32_t *seq_lens, int b, int maxp)
 {
@@ -163,39 +148,78 @@ __device__ inline int range_of(long long t, long long T, long long W)
     return (int)(((t + 1) * W - 1) / T);
 }
 
+template <typename T>
+__device__ inline T wave_inclusive_scan(T x, int lane)
+{
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const T y = __shfl_up(x, off);
+        if (lane >= off)
+            x += y;
+    }
+    return x;
+}
+
+// One workgroup.  Thread t owns requests [t * per, (t + 1) * per): a serial
+// prefix over its own requests, a wave scan of the per-thread totals and one
+// scan of the per-wave totals give every request's first tile and token.
 __global__ void __launch_bounds__(kPlanThreads)
 plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int forced,
             int resident_groups, char *__restrict__ ws, WsLayout lay)
 {
     __shared__ int s_pre[kMaxSeqs + 1];
-    __shared__ long long s_scan[kPlanThreads];
-    __shared__ int s_W;
-    const int t = threadIdx.x;
+    __shared__ int s_wtiles[kPlanThreads / 64];
+    __shared__ long long s_wtok[kPlanThreads / 64];
+    __shared__ int s_W, s_T, s_nmerge;
+    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
+    const int per = (B + kPlanThreads - 1) / kPlanThreads;
+    const int b0 = t * per;
 
-    int *tile_base = (int *)(ws + lay.tile_base);
-    long long *tok_base = (long long *)(ws + lay.tok_base);
-    int carry = 0;
-    long long tcarry = 0;
-    for (int b0 = 0; b0 < B; b0 += kPlanThreads) {
-        const int b = b0 + t;
-        const int L = b < B ? clamped_len(seq_lens, b, maxp) : 0;
-        const int tiles = (L + kPage - 1) / kPage * Hg;
-        long long tot_s, tot_t;
-        const long long ex_s = block_exclusive_scan<long long>(tiles, s_scan, tot_s);
-        const long long ex_t = block_exclusive_scan<long long>(L, s_scan, tot_t);
-        if (b < B) {
-            s_pre[b] = carry + (int)ex_s;
-            tile_base[b] = carry + (int)ex_s;
-            tok_base[b] = tcarry + ex_t;
-        }
-        carry += (int)tot_s;
-        tcarry += tot_t;
+    int tiles[kPlanPerThread];
+    int lens[kPlanPerThread];
+    int my_tiles = 0;
+    long long my_tok = 0;
+#pragma unroll
+    for (int k = 0; k < kPlanPerThread; ++k) {
+        const int b = b0 + k;
+        lens[k] = (k < per && b < B) ? clamped_len(seq_lens, b, maxp) : 0;
+        tiles[k] = (lens[k] + kPage - 1) / kPage * Hg;
+        my_tiles += tiles[k];
+        my_tok += lens[k];
     }
-    const int T = carry;
-    if (t == 0) {
+    const int inc_tiles = wave_inclusive_scan(my_tiles, lane);
+    const long long inc_tok = wave_inclusive_scan(my_tok, lane);
+    if (lane == 63) {
+        s_wtiles[wv] = inc_tiles;
+        s_wtok[wv] = inc_tok;
+    }
+    if (t == 0)
+        s_nmerge = 0;
+    __syncthreads();
+    int base_tiles = 0;
+    long long base_tok = 0;
+    for (int x = 0; x < wv; ++x) {
+        base_tiles += s_wtiles[x];
+        base_tok += s_wtok[x];
+    }
+    int pre = base_tiles + inc_tiles - my_tiles;
+    long long tpre = base_tok + inc_tok - my_tok;
+    long long *tok_base = (long long *)(ws + lay.tok_base);
+#pragma unroll
+    for (int k = 0; k < kPlanPerThread; ++k) {
+        const int b = b0 + k;
+        if (k < per && b < B) {
+            s_pre[b] = pre;
+            tok_base[b] = tpre;
+        }
+        pre += tiles[k];
+        tpre += lens[k];
+    }
+    if (t == kPlanThreads - 1) {
+        // the last thread's running sums are the totals
+        const int T = pre;
         s_pre[B] = T;
-        tile_base[B] = T;
-        tok_base[B] = tcarry;
+        tok_base[B] = tpre;
         long long W;
         if (T == 0) {
             W = 0;
@@ -208,12 +232,10 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
                 W = R * ceil_div_ll(T, (long long)kMaxRangeTiles * R);
         }
         s_W = (int)W;
-        PlanHeader *h = (PlanHeader *)(ws + lay.hdr);
-        h->n_ranges = (int)W;
-        h->n_tiles = T;
+        s_T = T;
     }
     __syncthreads();
-    const int W = s_W;
+    const int W = s_W, T = s_T;
 
     // range starts {b, q, j, t}; range W is the end sentinel
     int4 *ranges = (int4 *)(ws + lay.ranges);
@@ -233,18 +255,30 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
         ranges[w] = make_int4(lo, off / P, off % P, (int)tt);
     }
 
-    // per segment: first partial slot and number of pieces
+    // per segment: first partial slot and number of pieces; segments with
+    // other than exactly one piece (split, or empty request) go on the merge
+    // list for the combine kernel
     int2 *seg = (int2 *)(ws + lay.seg);
+    int4 *merge = (int4 *)(ws + lay.merge);
     for (int s = t; s < B * Hg; s += kPlanThreads) {
         const int b = s / Hg, q = s - (s / Hg) * Hg;
         const int P = (s_pre[b + 1] - s_pre[b]) / Hg;
-        if (P == 0) {
-            seg[s] = make_int2(0, 0);
-            continue;
+        int2 e = make_int2(0, 0);
+        if (P > 0) {
+            const long long t0 = s_pre[b] + (long long)q * P, t1 = t0 + P - 1;
+            const int w0 = range_of(t0, T, W), w1 = range_of(t1, T, W);
+            e = make_int2(w0 + s, w1 - w0 + 1);
         }
-        const long long t0 = s_pre[b] + (long long)q * P, t1 = t0 + P - 1;
-        const int w0 = range_of(t0, T, W), w1 = range_of(t1, T, W);
-        seg[s] = make_int2(w0 + s, w1 - w0 + 1);
+        seg[s] = e;
+        if (e.y != 1)
+            merge[atomicAdd(&s_nmerge, 1)] = make_int4(b, q, e.x, e.y);
+    }
+    __syncthreads();
+    if (t == 0) {
+        PlanHeader *h = (PlanHeader *)(ws + lay.hdr);
+        h->n_ranges = W;
+        h->n_tiles = T;
+        h->n_merge = s_nmerge;
     }
 }
 
@@ -596,71 +630,75 @@ attn_kernel(const AttnArgs a)
 // ---------------------------------------------------------------- combine
 struct CombineArgs {
     void *out;
-    const int2 *seg;
+    const PlanHeader *hdr;
+    const int4 *merge;
     const float2 *part_ml;
     const float *part_acc;
     int Hq, Hkv, G, HW;
 };
 
+// One workgroup per merge-list entry {b, q, first slot, pieces}
+// (grid-stride).  A segment's HW * G query heads times head_dim / 4 float4
+// chunks are spread over the threads; all of a chunk's partials are loaded
+// before any is used.  Empty requests get zeros.
+constexpr int kCombineUnroll = 4;
+
 template <int MODE>
 __global__ void __launch_bounds__(kCombineThreads)
 combine_kernel(const CombineArgs a)
 {
-    const int bh = blockIdx.x;
-    const int b = bh / a.Hq, h = bh - (bh / a.Hq) * a.Hq;
-    const int g = h / a.G, hh = h - g * a.G;
-    const int q = g / a.HW, hi = g - q * a.HW;
-    const int2 sg = a.seg[(size_t)b * (a.Hkv / a.HW) + q];
-    const int first = sg.x, n = sg.y;
-    if (n == 1)
-        return;   // the only piece wrote the output
-    const int lane = threadIdx.x;
-    float o0 = 0.f, o1 = 0.f;
-    if (n > 1) {
-        float M = -INFINITY;
-        for (int s = lane; s < n; s += 64)
-            M = fmaxf(M, a.part_ml[((size_t)(first + s) * a.HW + hi) * a.G + hh].x);
+    const int n_merge = a.hdr->n_merge;
+    const int G = a.G, HW = a.HW;
+    const int units = HW * G * (kHeadDim / 4);
+    for (int e = blockIdx.x; e < n_merge; e += gridDim.x) {
+        const int4 m = a.merge[e];
+        const int b = m.x, q = m.y, first = m.z, n = m.w;
+        for (int u = threadIdx.x; u < units; u += kCombineThreads) {
+            const int row = u / (kHeadDim / 4), c4 = u - row * (kHeadDim / 4);
+            const int hi = row / G, hh = row - hi * G;
+            f32x4 o = {0.f, 0.f, 0.f, 0.f};
+            if (n > 1) {
+                // running log-sum-exp over blocks of kCombineUnroll pieces
+                float M = -INFINITY, den = 0.f;
+                for (int p0 = 0; p0 < n; p0 += kCombineUnroll) {
+                    float2 ml[kCombineUnroll];
+                    f32x4 v[kCombineUnroll];
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1)
-            M = fmaxf(M, __shfl_xor(M, off));
-        float den = 0.f;
-        int s = 0;
-        for (; s + 4 <= n; s += 4) {
-            float2 ml[4];
-            float2 v[4];
+                    for (int k = 0; k < kCombineUnroll; ++k) {
+                        const int p = min(p0 + k, n - 1);
+                        const size_t it = ((size_t)(first + p) * HW + hi) * G + hh;
+                        ml[k] = a.part_ml[it];
+                        v[k] = *(const f32x4 *)(a.part_acc + it * kHeadDim + 4 * c4);
+                    }
+                    float Mb = M;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const size_t it = ((size_t)(first + s + u) * a.HW + hi) * a.G + hh;
-                ml[u] = a.part_ml[it];
-                v[u] = *(const float2 *)(a.part_acc + it * kHeadDim + 2 * lane);
+                    for (int k = 0; k < kCombineUnroll; ++k)
+                        if (p0 + k < n)
+                            Mb = fmaxf(Mb, ml[k].x);
+                    const float r = __builtin_amdgcn_exp2f(M - Mb);
+                    den *= r;
+                    o *= r;
+#pragma unroll
+                    for (int k = 0; k < kCombineUnroll; ++k) {
+                        if (p0 + k < n) {
+                            const float w = __builtin_amdgcn_exp2f(ml[k].x - Mb);
+                            den += w * ml[k].y;
+                            o += w * v[k];
+                        }
+                    }
+                    M = Mb;
+                }
+                o *= 1.0f / den;
             }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const float w = __builtin_amdgcn_exp2f(ml[u].x - M);
-                den += w * ml[u].y;
-                o0 += w * v[u].x;
-                o1 += w * v[u].y;
+            const size_t dst = ((size_t)b * a.Hq + (q * HW + hi) * G + hh) * kHeadDim + 4 * c4;
+            if constexpr (MODE == MODE_F32) {
+                *(f32x4 *)((float *)a.out + dst) = o;
+            } else {
+                *(u32x2 *)((uint16_t *)a.out + dst) =
+                    u32x2{(unsigned)bf16_bits(o[0]) | ((unsigned)bf16_bits(o[1]) << 16),
+                          (unsigned)bf16_bits(o[2]) | ((unsigned)bf16_bits(o[3]) << 16)};
             }
         }
-        for (; s < n; ++s) {
-            const size_t it = ((size_t)(first + s) * a.HW + hi) * a.G + hh;
-            const float2 ml = a.part_ml[it];
-            const float2 v = *(const float2 *)(a.part_acc + it * kHeadDim + 2 * lane);
-            const float w = __builtin_amdgcn_exp2f(ml.x - M);
-            den += w * ml.y;
-            o0 += w * v.x;
-            o1 += w * v.y;
-        }
-        const float inv = 1.0f / den;
-        o0 *= inv;
-        o1 *= inv;
-    }
-    if constexpr (MODE == MODE_F32) {
-        float *o = (float *)a.out + ((size_t)b * a.Hq + h) * kHeadDim + 2 * lane;
-        *(float2 *)o = make_float2(o0, o1);
-    } else {
-        uint16_t *o = (uint16_t *)a.out + ((size_t)b * a.Hq + h) * kHeadDim + 2 * lane;
-        *(unsigned *)o = (unsigned)bf16_bits(o0) | ((unsigned)bf16_bits(o1) << 16);
     }
 }
 
@@ -912,14 +950,19 @@ int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, in
     char *ws = (char *)workspace;
     CombineArgs c;
     c.out = out;
-    c.seg = (const int2 *)(ws + lay.seg);
+    c.hdr = (const PlanHeader *)(ws + lay.hdr);
+    c.merge = (const int4 *)(ws + lay.merge);
     c.part_ml = (const float2 *)(ws + lay.part_ml);
     c.part_acc = (const float *)(ws + lay.part_acc);
     c.Hq = n_q_heads;
     c.Hkv = n_kv_heads;
     c.G = G;
     c.HW = heads_per_group(n_kv_heads);
-    const dim3 grid((unsigned)num_seqs * n_q_heads);
+    int cus = 0;
+    st = num_cus(&cus);
+    if (st)
+        return st;
+    const dim3 grid((unsigned)(cus * kCombineGroupsPerCU));
     if (flags & VD_FLAG_OUT_F32)
         hipLaunchKernelGGL(combine_kernel<MODE_F32>, grid, dim3(kCombineThreads), 0, stream, c);
     else
