@@ -53,6 +53,117 @@ def committed_traffic(workload: str):
     return t.get("hbm_bytes_per_launch")
 
 
+SURFACE_BATCH = (1, 2, 4, 8, 16, 32, 64, 128, 256, 512)
+SURFACE_LEN = (16, 64, 256, 1024, 4096, 16384)
+SURFACE_GQA8_BATCH = (64, 128, 256)
+
+
+def latency_surface(outdir: str, iters: int = 10, warmup: int = 3):
+    """Step time over (N_req, N_kv): the state the paper's decode-latency
+    model consumes (Sec. 5.4, Eq. pred-itl).  Grid: batch x tokens per
+    request, equal lengths and a lognormal-ragged mix of the same mean
+    (sigma 0.8, clipped to [1, 4 x mean]); plus 64:8 heads at a few batches.
+    Values are random bf16 drawn on the GPU (timing only; parity is covered by
+    the tests).  Fits T = c*N_req + d*N_kv + e by least squares."""
+    import numpy as np
+    import torch
+
+    import paper_2509_04827_amd as vd
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    gen = torch.Generator(device=dev).manual_seed(0)
+    rng = np.random.default_rng(0)
+    Hkv, D, S = 8, 128, 16
+    max_tokens = max(SURFACE_BATCH) * max(SURFACE_LEN) * 4 // 3
+    max_pages = max_tokens // S + max(SURFACE_BATCH) + 1
+    kp = torch.randn((max_pages, S, Hkv, D), generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    vp = torch.randn((max_pages, S, Hkv, D), generator=gen, device=dev, dtype=torch.float32).to(torch.bfloat16)
+    stream = torch.cuda.current_stream()
+    rows = []
+
+    def point(B, lens, Hq, law):
+        lens = np.asarray(lens, dtype=np.int64)
+        P = (lens + S - 1) // S
+        if P.sum() > max_pages:
+            return
+        maxp = int(max(1, P.max()))
+        perm = rng.permutation(max_pages)[:int(P.sum())].astype(np.int32)
+        pt = np.zeros((B, maxp), dtype=np.int32)
+        off = 0
+        for b in range(B):
+            pt[b, :P[b]] = perm[off:off + P[b]]
+            off += int(P[b])
+        q = torch.randn((B, Hq, D), generator=gen, device=dev).to(torch.bfloat16)
+        out = torch.empty_like(q)
+        ptd = torch.from_numpy(pt).to(dev)
+        sl = torch.from_numpy(lens.astype(np.int32)).to(dev)
+        ws = vd.alloc_workspace(B, Hq, Hkv, maxp)
+        scale = float(np.float32(1.0 / np.sqrt(D)))
+
+        def step(e0=None, e1=None):
+            vd.vd_decode_plan(sl, Hq, Hkv, maxp, ws, stream=stream)
+            if e0 is not None:
+                e0.record(stream)
+            vd.vd_decode_partial(q, kp, vp, ptd, sl, out, scale, ws, stream=stream)
+            if e1 is not None:
+                e1.record(stream)
+            vd.vd_decode_combine(out, Hkv, maxp, ws, stream=stream)
+
+        for _ in range(warmup):
+            step()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(iters)]
+        st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        st.record(stream)
+        for e0, e1 in ev:
+            step(e0, e1)
+        en.record(stream)
+        torch.cuda.synchronize()
+        us_step = st.elapsed_time(en) * 1e3 / iters
+        us_attn = float(np.median([a.elapsed_time(b) for a, b in ev])) * 1e3
+        n_kv = int(lens.sum())
+        kvb = n_kv * Hkv * D * 2 * 2
+        rows.append(dict(law=law, n_q_heads=Hq, n_req=B, tokens_per_req=int(round(lens.mean())),
+                         n_kv=n_kv, us_step=round(us_step, 2), us_attn=round(us_attn, 2),
+                         kv_gbs_step=round(kvb / us_step / 1e3, 1)))
+        print("surface %-8s Hq %2d B %4d L %6d N_kv %8d  step %9.2f us  attn %9.2f us  %7.1f GB/s"
+              % (law, Hq, B, lens.mean(), n_kv, us_step, us_attn, kvb / us_step / 1e3),
+              file=sys.stderr, flush=True)
+
+    for B in SURFACE_BATCH:
+        for L in SURFACE_LEN:
+            point(B, [L] * B, 32, "equal")
+            z = rng.standard_normal(B)
+            lens = np.clip(np.round(L * np.exp(0.8 * z - 0.32)), 1, 4 * L)
+            point(B, lens, 32, "ragged")
+    for B in SURFACE_GQA8_BATCH:
+        for L in SURFACE_LEN:
+            point(B, [L] * B, 64, "equal")
+
+    os.makedirs(outdir, exist_ok=True)
+    keys = list(rows[0].keys())
+    with open(os.path.join(outdir, "decode_latency_surface.csv"), "w") as f:
+        f.write(",".join(keys) + "\n")
+        for r in rows:
+            f.write(",".join(str(r[k]) for k in keys) + "\n")
+    # Eq. pred-itl: T = c*N_req + d*N_kv + e, fitted on the 32:8 points
+    sel = [r for r in rows if r["n_q_heads"] == 32]
+    A = np.array([[r["n_req"], r["n_kv"], 1.0] for r in sel], dtype=np.float64)
+    y = np.array([r["us_step"] for r in sel])
+    coef, *_ = np.linalg.lstsq(A, y, rcond=None)
+    pred = A @ coef
+    r2 = 1.0 - ((y - pred) ** 2).sum() / ((y - y.mean()) ** 2).sum()
+    mae = float(np.abs(y - pred).mean())
+    bw = Hkv * D * 2 * 2 / (coef[1] * 1e-6) / 1e9
+    fit = dict(c_us_per_req=coef[0], d_us_per_kv_token=coef[1], e_us=coef[2], r2=r2, mae_us=mae,
+               implied_kv_gbs=bw, points=len(sel))
+    with open(os.path.join(outdir, "decode_latency_surface_fit.json"), "w") as f:
+        json.dump(fit, f, indent=1)
+    print(json.dumps({"surface_points": len(rows), "fit": fit}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -65,6 +176,9 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after timing, copy a BYTES-sized buffer 3 times (a plain copy "
                          "kernel of known size, to scale HBM counters by)")
+    ap.add_argument("--surface", metavar="DIR", default=None,
+                    help="instead of the bench line, measure the latency surface over "
+                         "(batch, tokens per request) and write DIR/decode_latency_surface.{csv,md}")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -79,6 +193,10 @@ def main():
 
     import paper_2509_04827_amd as vd
     from workloads import WORKLOADS, bits, kv_bytes, make_case
+
+    if args.surface:
+        latency_surface(args.surface)
+        return
 
     w = WORKLOADS[args.workload]
     t0 = time.time()

@@ -66,7 +66,7 @@ constexpr int kPrefetch = 2;           // pages in flight per wave (ring of page
 constexpr int kMaxHeadsPerGroup = 8;
 constexpr int kAttnMaxThreads = 64 * kMaxHeadsPerGroup;
 constexpr int kCombineThreads = 256;
-constexpr int kCombineGroupsPerCU = 2;
+constexpr int kCombineGroupsPerCU = 4;
 constexpr float kLog2e = 1.4426950408889634f;
 // Lazy rescaling: the running max is only raised when a new score exceeds it
 // by more than this (log2 units), so weights stay below 2^8 and acc/l never
@@ -637,68 +637,94 @@ struct CombineArgs {
     int Hq, Hkv, G, HW;
 };
 
-// One workgroup per merge-list entry {b, q, first slot, pieces}
-// (grid-stride).  A segment's HW * G query heads times head_dim / 4 float4
-// chunks are spread over the threads; all of a chunk's partials are loaded
-// before any is used.  Empty requests get zeros.
+// Work items are (merge-list entry {b, q, first slot, pieces}, query head of
+// the segment); workgroups stride over them.  A workgroup's 256 threads are
+// 32 float4 chunks of head_dim times kCombineLanes piece lanes: lane l merges
+// pieces l, l + kCombineLanes, ... (running log-sum-exp, kCombineUnroll loads
+// in flight), then the lanes' (max, normaliser, accumulator) are merged in
+// LDS.  Empty requests get zeros.
+constexpr int kCombineLanes = kCombineThreads / (kHeadDim / 4);
 constexpr int kCombineUnroll = 4;
 
 template <int MODE>
 __global__ void __launch_bounds__(kCombineThreads)
 combine_kernel(const CombineArgs a)
 {
+    __shared__ float s_m[kCombineLanes][kHeadDim / 4];
+    __shared__ float s_l[kCombineLanes][kHeadDim / 4];
+    __shared__ f32x4 s_o[kCombineLanes][kHeadDim / 4];
     const int n_merge = a.hdr->n_merge;
     const int G = a.G, HW = a.HW;
-    const int units = HW * G * (kHeadDim / 4);
-    for (int e = blockIdx.x; e < n_merge; e += gridDim.x) {
+    const int rows = HW * G;
+    const int c4 = threadIdx.x & (kHeadDim / 4 - 1);
+    const int pl = threadIdx.x / (kHeadDim / 4);
+    for (int item = blockIdx.x; item < n_merge * rows; item += gridDim.x) {
+        const int e = item / rows, row = item - (item / rows) * rows;
         const int4 m = a.merge[e];
         const int b = m.x, q = m.y, first = m.z, n = m.w;
-        for (int u = threadIdx.x; u < units; u += kCombineThreads) {
-            const int row = u / (kHeadDim / 4), c4 = u - row * (kHeadDim / 4);
-            const int hi = row / G, hh = row - hi * G;
-            f32x4 o = {0.f, 0.f, 0.f, 0.f};
-            if (n > 1) {
-                // running log-sum-exp over blocks of kCombineUnroll pieces
-                float M = -INFINITY, den = 0.f;
-                for (int p0 = 0; p0 < n; p0 += kCombineUnroll) {
-                    float2 ml[kCombineUnroll];
-                    f32x4 v[kCombineUnroll];
+        const int hi = row / G, hh = row - hi * G;
+        float M = -INFINITY, den = 0.f;
+        f32x4 o = {0.f, 0.f, 0.f, 0.f};
+        for (int p0 = pl; p0 < n; p0 += kCombineLanes * kCombineUnroll) {
+            float2 ml[kCombineUnroll];
+            f32x4 v[kCombineUnroll];
 #pragma unroll
-                    for (int k = 0; k < kCombineUnroll; ++k) {
-                        const int p = min(p0 + k, n - 1);
-                        const size_t it = ((size_t)(first + p) * HW + hi) * G + hh;
-                        ml[k] = a.part_ml[it];
-                        v[k] = *(const f32x4 *)(a.part_acc + it * kHeadDim + 4 * c4);
-                    }
-                    float Mb = M;
+            for (int k = 0; k < kCombineUnroll; ++k) {
+                const int p = min(p0 + k * kCombineLanes, n - 1);
+                const size_t it = ((size_t)(first + p) * HW + hi) * G + hh;
+                ml[k] = a.part_ml[it];
+                v[k] = *(const f32x4 *)(a.part_acc + it * kHeadDim + 4 * c4);
+            }
+            float Mb = M;
 #pragma unroll
-                    for (int k = 0; k < kCombineUnroll; ++k)
-                        if (p0 + k < n)
-                            Mb = fmaxf(Mb, ml[k].x);
-                    const float r = __builtin_amdgcn_exp2f(M - Mb);
-                    den *= r;
-                    o *= r;
+            for (int k = 0; k < kCombineUnroll; ++k)
+                if (p0 + k * kCombineLanes < n)
+                    Mb = fmaxf(Mb, ml[k].x);
+            const float r = __builtin_amdgcn_exp2f(M - Mb);
+            den *= r;
+            o *= r;
 #pragma unroll
-                    for (int k = 0; k < kCombineUnroll; ++k) {
-                        if (p0 + k < n) {
-                            const float w = __builtin_amdgcn_exp2f(ml[k].x - Mb);
-                            den += w * ml[k].y;
-                            o += w * v[k];
-                        }
-                    }
-                    M = Mb;
+            for (int k = 0; k < kCombineUnroll; ++k) {
+                if (p0 + k * kCombineLanes < n) {
+                    const float w = __builtin_amdgcn_exp2f(ml[k].x - Mb);
+                    den += w * ml[k].y;
+                    o += w * v[k];
                 }
-                o *= 1.0f / den;
+            }
+            M = Mb;
+        }
+        s_m[pl][c4] = M;
+        s_l[pl][c4] = den;
+        s_o[pl][c4] = o;
+        __syncthreads();
+        if (pl == 0) {
+            f32x4 res = {0.f, 0.f, 0.f, 0.f};
+            if (n > 1) {
+                float Mt = -INFINITY;
+#pragma unroll
+                for (int x = 0; x < kCombineLanes; ++x)
+                    Mt = fmaxf(Mt, s_m[x][c4]);
+                float dt = 0.f;
+#pragma unroll
+                for (int x = 0; x < kCombineLanes; ++x) {
+                    if (x < n) {   // lanes without pieces hold M = -inf
+                        const float w = __builtin_amdgcn_exp2f(s_m[x][c4] - Mt);
+                        dt += w * s_l[x][c4];
+                        res += w * s_o[x][c4];
+                    }
+                }
+                res *= 1.0f / dt;
             }
             const size_t dst = ((size_t)b * a.Hq + (q * HW + hi) * G + hh) * kHeadDim + 4 * c4;
             if constexpr (MODE == MODE_F32) {
-                *(f32x4 *)((float *)a.out + dst) = o;
+                *(f32x4 *)((float *)a.out + dst) = res;
             } else {
                 *(u32x2 *)((uint16_t *)a.out + dst) =
-                    u32x2{(unsigned)bf16_bits(o[0]) | ((unsigned)bf16_bits(o[1]) << 16),
-                          (unsigned)bf16_bits(o[2]) | ((unsigned)bf16_bits(o[3]) << 16)};
+                    u32x2{(unsigned)bf16_bits(res[0]) | ((unsigned)bf16_bits(res[1]) << 16),
+                          (unsigned)bf16_bits(res[2]) | ((unsigned)bf16_bits(res[3]) << 16)};
             }
         }
+        __syncthreads();
     }
 }
 

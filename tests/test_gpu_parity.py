@@ -217,6 +217,18 @@ def test_split_invariance():
             check_f32(got, ref, "split %d" % s)
 
 
+@pytest.mark.parametrize("lengths", [[16384], [60000, 3], [131072]])
+def test_few_long_requests(lengths):
+    """Few long requests: every CU takes a slice of them, so each (request,
+    head group) is split into many pieces that the combine must merge."""
+    say("case: long requests %s" % lengths)
+    c = custom(lengths, seed=20 + len(lengths))
+    d = dev_case(c)
+    ref = ref_of(c)
+    check_f32(run_gpu(d), ref, "long %s" % lengths)
+    check_bf16(run_gpu(d, torch.bfloat16), ref, "long %s" % lengths)
+
+
 def test_pt_stride():
     say("case: wide page-table rows")
     c = custom([100, 7, 900], seed=10, pt_stride=200)
