@@ -1,0 +1,91 @@
+"""Decode-attention latency model over (N_req, N_kv), fitted to measurements.
+
+The paper's iteration-level controller needs the decode iteration time as a
+function of the system state: EcoPred models it as T_D ~ c_f * N_req +
+d_f * N_kv + e_f within a GEMM tile (Sec. 5.4, Eq. pred-itl), with N_kv
+driving the attention layer and its KV-cache reads, and fits a boosted-tree
+regressor on (f, N_req, N_kv) for accuracy (Sec. 5.4; decode model settings in
+the appendix on its XGBoost configuration: absolute-error objective, 1000
+rounds, learning rate 0.1, depth 6, early stopping after 200 rounds).
+
+Here the same two models are fitted to the step times this library's
+decode-attention path measures on MI355X at its fixed clock (the latency
+surface written by ``bench.py --surface``).  CPU only; it consumes the
+measurements and launches nothing.  XGBoost is not available in this
+environment, so the boosted model is scikit-learn's histogram gradient
+boosting with the same objective, rate, depth, round budget and patience
+(it has no row/column subsampling).
+"""
+from __future__ import annotations
+
+import csv
+from dataclasses import dataclass
+
+import numpy as np
+
+
+@dataclass
+class LinearFit:
+    """T = c * n_req + d * n_kv + e (microseconds)."""
+    c: float
+    d: float
+    e: float
+    r2: float
+    mae: float
+
+    def predict(self, n_req, n_kv):
+        return self.c * np.asarray(n_req, float) + self.d * np.asarray(n_kv, float) + self.e
+
+    def kv_bandwidth_gbs(self, kv_bytes_per_token: int = 4096) -> float:
+        """Bandwidth implied by the marginal cost of one KV token."""
+        return kv_bytes_per_token / (self.d * 1e-6) / 1e9
+
+
+def load_surface(path: str, n_q_heads: int | None = 32):
+    """Rows of a latency-surface CSV as (n_req, n_kv, us_step) arrays."""
+    with open(path) as f:
+        rows = [r for r in csv.DictReader(f)
+                if n_q_heads is None or int(r["n_q_heads"]) == n_q_heads]
+    n_req = np.array([int(r["n_req"]) for r in rows], float)
+    n_kv = np.array([int(r["n_kv"]) for r in rows], float)
+    t = np.array([float(r["us_step"]) for r in rows], float)
+    return n_req, n_kv, t
+
+
+def fit_linear(n_req, n_kv, t) -> LinearFit:
+    n_req, n_kv, t = (np.asarray(x, float) for x in (n_req, n_kv, t))
+    A = np.stack([n_req, n_kv, np.ones_like(t)], axis=1)
+    coef, *_ = np.linalg.lstsq(A, t, rcond=None)
+    pred = A @ coef
+    ss = ((t - t.mean()) ** 2).sum()
+    r2 = 1.0 - ((t - pred) ** 2).sum() / ss if ss > 0 else 1.0
+    return LinearFit(float(coef[0]), float(coef[1]), float(coef[2]), float(r2),
+                     float(np.abs(t - pred).mean()))
+
+
+def fit_boosted(n_req, n_kv, t, random_state: int = 42):
+    """Boosted trees on (n_req, n_kv) with the decode settings of the paper."""
+    from sklearn.ensemble import HistGradientBoostingRegressor
+
+    X = np.stack([np.asarray(n_req, float), np.asarray(n_kv, float)], axis=1)
+    model = HistGradientBoostingRegressor(
+        loss="absolute_error", learning_rate=0.1, max_iter=1000, max_depth=6,
+        early_stopping=True, n_iter_no_change=200, validation_fraction=0.2,
+        random_state=random_state)
+    model.fit(X, np.asarray(t, float))
+    return model
+
+
+def holdout_mae(n_req, n_kv, t, test_fraction: float = 0.25, seed: int = 0):
+    """MAE of both models on a random held-out share of the points."""
+    n_req, n_kv, t = (np.asarray(x, float) for x in (n_req, n_kv, t))
+    rng = np.random.default_rng(seed)
+    idx = rng.permutation(t.shape[0])
+    k = max(1, int(round(test_fraction * t.shape[0])))
+    te, tr = idx[:k], idx[k:]
+    lin = fit_linear(n_req[tr], n_kv[tr], t[tr])
+    gb = fit_boosted(n_req[tr], n_kv[tr], t[tr])
+    lin_mae = float(np.abs(lin.predict(n_req[te], n_kv[te]) - t[te]).mean())
+    gb_mae = float(np.abs(gb.predict(np.stack([n_req[te], n_kv[te]], 1)) - t[te]).mean())
+    return {"linear_mae_us": lin_mae, "boosted_mae_us": gb_mae, "n_train": int(tr.size),
+            "n_test": int(te.size)}

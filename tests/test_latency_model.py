@@ -1,0 +1,38 @@
+"""Decode latency model (Eq. pred-itl fit and boosted trees) on synthetic data."""
+import numpy as np
+
+from paper_2509_04827_amd import latency_model as lm
+
+
+def grid():
+    n_req = np.repeat([1, 2, 4, 8, 16, 32, 64, 128, 256, 512], 6).astype(float)
+    n_kv = n_req * np.tile([16, 64, 256, 1024, 4096, 16384], 10)
+    return n_req, n_kv
+
+
+def test_linear_fit_recovers_coefficients():
+    n_req, n_kv = grid()
+    t = 0.02 * n_req + 6.25e-4 * n_kv + 21.5
+    f = lm.fit_linear(n_req, n_kv, t)
+    assert abs(f.c - 0.02) < 1e-9 and abs(f.d - 6.25e-4) < 1e-12 and abs(f.e - 21.5) < 1e-7
+    assert f.r2 > 1 - 1e-12 and f.mae < 1e-7
+    # 4096 B of KV per token at 6.25e-4 us per token is 6.5536 TB/s
+    assert abs(f.kv_bandwidth_gbs() - 6553.6) < 1e-6
+
+
+def test_boosted_beats_constant_on_dense_data():
+    rng = np.random.default_rng(0)
+    n_req = rng.integers(1, 512, 4000).astype(float)
+    n_kv = n_req * rng.integers(16, 4096, 4000)
+    t = 0.02 * n_req + 6.25e-4 * n_kv + 21.5 + rng.normal(0, 1, 4000)
+    m = lm.fit_boosted(n_req[:3000], n_kv[:3000], t[:3000])
+    pred = m.predict(np.stack([n_req[3000:], n_kv[3000:]], 1))
+    mae = np.abs(pred - t[3000:]).mean()
+    assert mae < 0.1 * np.abs(t[3000:] - np.median(t[:3000])).mean()
+
+
+def test_holdout_reports_both():
+    n_req, n_kv = grid()
+    t = 0.02 * n_req + 6.25e-4 * n_kv + 21.5
+    r = lm.holdout_mae(n_req, n_kv, t)
+    assert r["linear_mae_us"] < 1e-6 and r["n_test"] + r["n_train"] == 60
