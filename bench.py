@@ -14,6 +14,8 @@ Prints one JSON line:
                 MI355X's 8 TB/s; traffic from the committed FETCH_SIZE /
                 WRITE_SIZE counter summary when it matches this kernel source
   cpu_baseline  the fp64 oracle on the host cores over the same workload
+  cold_cache    step times with a 1 GiB cache flush before each step
+                (p10 / median / p90), outside the back-to-back timing
 """
 from __future__ import annotations
 
@@ -171,6 +173,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-cold", action="store_true", help="skip the flushed-cache step timings")
+    ap.add_argument("--no-ceiling", action="store_true", help="skip the HBM read-ceiling run")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="stop repeating the oracle after this much wall time")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -247,6 +251,44 @@ def main():
     attn_ms = [a0[i].elapsed_time(a1[i]) for i in range(K)]
     attn_avg_ms = float(np.mean(attn_ms))
 
+    # Cold caches: a 1 GiB write (beyond the 256 MB Infinity Cache and the
+    # L2s) before each step; per-step events, outside the back-to-back timing.
+    cold = None
+    if not args.no_cold:
+        flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)
+        steps_us, attn_us = [], []
+        for _ in range(max(10, K // 2)):
+            flush.zero_()
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+            e[0].record(stream)
+            step(e[1], e[2])
+            e[3].record(stream)
+            torch.cuda.synchronize()
+            steps_us.append(e[0].elapsed_time(e[3]) * 1e3)
+            attn_us.append(e[1].elapsed_time(e[2]) * 1e3)
+        del flush
+        p10, p50, p90 = np.percentile(steps_us, [10, 50, 90])
+        cold = {"flush_bytes": 1 << 30, "us_per_step_p10": round(float(p10), 2),
+                "us_per_step_median": round(float(p50), 2), "us_per_step_p90": round(float(p90), 2),
+                "attn_us_median": round(float(np.median(attn_us)), 2),
+                "kv_gbs_median": round(kv_bytes(c) / (p50 * 1e-6) / 1e9, 2)}
+
+    # HBM read ceiling on this device: vd_stream_read over 4 GiB.
+    ceiling = None
+    if not args.no_ceiling:
+        buf = torch.zeros(1 << 32, dtype=torch.uint8, device=dev)
+        sink = torch.zeros(4, dtype=torch.int32, device=dev)
+        for _ in range(2):
+            vd.vd_stream_read(buf, sink, stream=stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(5):
+            vd.vd_stream_read(buf, sink, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ceiling = round((1 << 32) * 5 / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+        del buf, sink
+
     if args.copy_calibration:
         n = args.copy_calibration // 4
         src = torch.ones(n, dtype=torch.int32, device=dev)
@@ -303,7 +345,10 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                      "traffic": traffic, "kernel": "attn_kernel",
-                     "algorithmic_bytes": algo_bytes, "avg_launch_us": round(attn_avg_ms * 1e3, 2)},
+                     "algorithmic_bytes": algo_bytes, "avg_launch_us": round(attn_avg_ms * 1e3, 2),
+                     "stream_read_ceiling_gbs": ceiling,
+                     "frac_of_stream_ceiling": round(achieved / ceiling, 4) if ceiling else None},
+        "cold_cache": cold,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -154,6 +154,35 @@ int vd_decode_gather(const void *k_pages, const void *v_pages,
                      void *workspace, size_t workspace_bytes,
                      hipStream_t stream);
 
+/*
+ * Append the current token of every request to the paged KV cache, the step
+ * that precedes attention in a decode iteration (the newest token's K/V are
+ * cached before the step attends to all L_b tokens; Sec. 5.4 counts them in
+ * N_kv).  For each request b with 0 <= positions[b] < max_pages_per_seq *
+ * page_size, copies k_new[b] and v_new[b] (bf16 [num_seqs][n_kv_heads]
+ * [head_dim], 16-byte aligned) into row positions[b] mod page_size of page
+ * page_table[b][positions[b] / page_size] of k_pages / v_pages (layouts as
+ * above); other requests are skipped.  Bit-exact copies.  The page table
+ * entry for that position must name a valid page (precondition).  Sizes as
+ * vd_decode_gather (head_dim 128, page_size 16).
+ */
+int vd_kv_append(const void *k_new, const void *v_new, void *k_pages,
+                 void *v_pages, const int32_t *page_table,
+                 const int32_t *positions, int num_seqs, int n_kv_heads,
+                 int head_dim, int page_size, int max_pages_per_seq,
+                 hipStream_t stream);
+
+/*
+ * Measurement aid, not part of the attention path: reads `bytes` (a multiple
+ * of 16) from device buffer `buf` with 16-byte non-temporal loads from
+ * `blocks` workgroups of 256 threads, and may write 4 bytes to device pointer
+ * `sink` (so the reads cannot be optimised away).  Timing it gives the HBM
+ * read rate this device sustains, the practical ceiling for vd_decode_attn.
+ * buf 16-byte aligned, sink 4-byte aligned, blocks > 0.
+ */
+int vd_stream_read(const void *buf, size_t bytes, void *sink, int blocks,
+                   hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -55,6 +55,8 @@ def _load():
         lib.vdo_decode_attn_rows_f64.restype = I
         lib.vdo_gather.argtypes = [P, P, P, P, P, P, I, I, I, I, I]
         lib.vdo_gather.restype = I
+        lib.vdo_kv_append.argtypes = [P, P, P, P, P, P, I, I, I, I, I]
+        lib.vdo_kv_append.restype = I
         lib.vdo_softmax_f64.argtypes = [P, I, P]
         lib.vdo_softmax_f64.restype = None
         lib.vdo_max_threads.argtypes = []
@@ -142,6 +144,21 @@ def gather(k_pages, v_pages, page_table, seq_lens):
     if rc != 0:
         raise RuntimeError("oracle vdo_gather failed with code %d" % rc)
     return k_out, v_out
+
+
+def kv_append(k_new, v_new, k_pages, v_pages, page_table, positions) -> None:
+    """In place: write k_new[b] / v_new[b] (uint16 [B][Hkv][D]) at token
+    positions[b] of request b's pages; negative or out-of-table positions skip."""
+    k_new, v_new = _u16(k_new), _u16(v_new)
+    page_table, positions = _i32(page_table), _i32(positions)
+    assert k_pages.flags.c_contiguous and v_pages.flags.c_contiguous
+    assert k_pages.dtype == np.uint16 and v_pages.dtype == np.uint16
+    _, S, Hkv, D = k_pages.shape
+    rc = _load().vdo_kv_append(_ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages),
+                               _ptr(page_table), _ptr(positions), positions.shape[0], Hkv, D, S,
+                               page_table.shape[1])
+    if rc != 0:
+        raise RuntimeError("oracle vdo_kv_append failed with code %d" % rc)
 
 
 def softmax(s) -> np.ndarray:

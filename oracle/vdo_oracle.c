@@ -34,7 +34,8 @@
  *
  * Parity status: pinned by the not-gpu tests (brute force, L = 1, constant V,
  * shift invariance, page-permutation invariance, closed forms, GQA vs
- * duplicated MHA, one-hot, float64 SDPA of a library).
+ * duplicated MHA, one-hot, float64 SDPA of a library; the gather and the KV
+ * append by direct indexing of the pools).
  */
 #include <math.h>
 #include <stdint.h>
@@ -215,6 +216,32 @@ int vdo_gather(const uint16_t *k_pages, const uint16_t *v_pages,
             memcpy(v_out + dst, v_pages + src, row * sizeof(uint16_t));
             dst += row;
         }
+    }
+    return 0;
+}
+
+/*
+ * Append one token per request: copy k_new[b] / v_new[b] (uint16
+ * [B][Hkv][D]) into row (pos mod S) of page page_table[b][pos / S] of the
+ * pools, pos = positions[b]; requests with pos < 0 or pos >= max_pages * S
+ * are skipped.  Pure byte copies.
+ */
+int vdo_kv_append(const uint16_t *k_new, const uint16_t *v_new, uint16_t *k_pages,
+                  uint16_t *v_pages, const int32_t *page_table, const int32_t *positions,
+                  int num_seqs, int n_kv_heads, int head_dim, int page_size,
+                  int max_pages_per_seq)
+{
+    if (num_seqs < 0 || n_kv_heads <= 0 || head_dim <= 0 || page_size <= 0)
+        return 1;
+    const size_t row = (size_t)n_kv_heads * head_dim;
+    for (int b = 0; b < num_seqs; ++b) {
+        const int pos = positions[b];
+        if (pos < 0 || pos >= max_pages_per_seq * page_size)
+            continue;
+        const int32_t p = page_table[(size_t)b * max_pages_per_seq + pos / page_size];
+        const size_t dst = (size_t)p * page_size * row + (size_t)(pos % page_size) * row;
+        memcpy(k_pages + dst, k_new + (size_t)b * row, row * sizeof(uint16_t));
+        memcpy(v_pages + dst, v_new + (size_t)b * row, row * sizeof(uint16_t));
     }
     return 0;
 }

@@ -36,7 +36,7 @@ VD_FLAG_OUT_F32 = 1 << 0
 VD_FLAG_RANGE_SHIFT = 8
 
 EXPORTS = ("vd_status_string", "vd_decode_workspace_size", "vd_decode_attn", "vd_decode_plan",
-           "vd_decode_partial", "vd_decode_combine", "vd_decode_gather")
+           "vd_decode_partial", "vd_decode_combine", "vd_decode_gather", "vd_kv_append", "vd_stream_read")
 
 
 def VD_FLAG_RANGE_TILES(n: int) -> int:
@@ -71,8 +71,9 @@ def lib() -> ctypes.CDLL:
         L.vd_decode_plan.argtypes = [P, I, I, I, I, I, I, P, Z, U, P]
         L.vd_decode_combine.argtypes = [P, I, I, I, I, I, I, P, Z, U, P]
         L.vd_decode_gather.argtypes = [P, P, P, P, P, P, I, I, I, I, I, P, Z, P]
+        L.vd_stream_read.argtypes = [P, Z, P, I, P]
         for n in ("vd_decode_attn", "vd_decode_partial", "vd_decode_plan", "vd_decode_combine",
-                  "vd_decode_gather"):
+                  "vd_decode_gather", "vd_kv_append", "vd_stream_read"):
             getattr(L, n).restype = I
         _lib = L
     return _lib
@@ -163,3 +164,17 @@ def vd_decode_gather(k_pages, v_pages, page_table, seq_lens, k_out, v_out, works
                                   _ptr(k_out), _ptr(v_out), seq_lens.shape[0], Hkv, D, S,
                                   page_table.shape[1], _ptr(workspace), workspace.numel(),
                                   _stream(stream)), "vd_decode_gather")
+
+
+def vd_kv_append(k_new, v_new, k_pages, v_pages, page_table, positions, stream=None) -> None:
+    """Write k_new[b] / v_new[b] at token positions[b] of request b's pages."""
+    _, S, Hkv, D = k_pages.shape
+    _check(lib().vd_kv_append(_ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages),
+                              _ptr(page_table), _ptr(positions), positions.shape[0], Hkv, D, S,
+                              page_table.shape[1], _stream(stream)), "vd_kv_append")
+
+
+def vd_stream_read(buf, sink, blocks: int = 8192, stream=None) -> None:
+    """Read all of `buf` (a measurement of the HBM read rate; see the header)."""
+    _check(lib().vd_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), int(blocks),
+                                _stream(stream)), "vd_stream_read")

@@ -82,8 +82,9 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 struct PlanHeader {
     int n_ranges;  // W
     int n_tiles;   // T
-    int n_merge;   // entries of the merge list
-    int pad[5];
+    int n_short;   // merge-list entries with at most kShortMerge pieces (front of the list)
+    int n_long;    // entries with more pieces (back of the list)
+    int pad[4];
 };
 
 // ---------------------------------------------------------------- workspace
@@ -135,6 +136,7 @@ inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced)
 
 // ---------------------------------------------------------------- planner
 constexpr int kPlanPerThread = kMaxSeqs / kPlanThreads;   // requests per planner thread
+constexpr int kShortMerge = 8;         // merge entries with more pieces take the piece-lane path
 
 __device__ inline int clamped_len(const int32_t *seq_lens, int b, int maxp)
 {
@@ -170,7 +172,7 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
     __shared__ int s_pre[kMaxSeqs + 1];
     __shared__ int s_wtiles[kPlanThreads / 64];
     __shared__ long long s_wtok[kPlanThreads / 64];
-    __shared__ int s_W, s_T, s_nmerge;
+    __shared__ int s_W, s_T, s_nshort, s_nlong;
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     const int per = (B + kPlanThreads - 1) / kPlanThreads;
     const int b0 = t * per;
@@ -193,8 +195,10 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
         s_wtiles[wv] = inc_tiles;
         s_wtok[wv] = inc_tok;
     }
-    if (t == 0)
-        s_nmerge = 0;
+    if (t == 0) {
+        s_nshort = 0;
+        s_nlong = 0;
+    }
     __syncthreads();
     int base_tiles = 0;
     long long base_tok = 0;
@@ -257,7 +261,8 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
 
     // per segment: first partial slot and number of pieces; segments with
     // other than exactly one piece (split, or empty request) go on the merge
-    // list for the combine kernel
+    // list for the combine kernel: up to kShortMerge pieces from the front,
+    // more from the back
     int2 *seg = (int2 *)(ws + lay.seg);
     int4 *merge = (int4 *)(ws + lay.merge);
     for (int s = t; s < B * Hg; s += kPlanThreads) {
@@ -270,15 +275,20 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
             e = make_int2(w0 + s, w1 - w0 + 1);
         }
         seg[s] = e;
-        if (e.y != 1)
-            merge[atomicAdd(&s_nmerge, 1)] = make_int4(b, q, e.x, e.y);
+        if (e.y != 1) {
+            if (e.y <= kShortMerge)
+                merge[atomicAdd(&s_nshort, 1)] = make_int4(b, q, e.x, e.y);
+            else
+                merge[B * Hg - 1 - atomicAdd(&s_nlong, 1)] = make_int4(b, q, e.x, e.y);
+        }
     }
     __syncthreads();
     if (t == 0) {
         PlanHeader *h = (PlanHeader *)(ws + lay.hdr);
         h->n_ranges = W;
         h->n_tiles = T;
-        h->n_merge = s_nmerge;
+        h->n_short = s_nshort;
+        h->n_long = s_nlong;
     }
 }
 
@@ -631,20 +641,75 @@ attn_kernel(const AttnArgs a)
 struct CombineArgs {
     void *out;
     const PlanHeader *hdr;
-    const int4 *merge;
+    const int4 *merge;      // short entries from the front, long ones from the back
     const float2 *part_ml;
     const float *part_acc;
-    int Hq, Hkv, G, HW;
+    int Hq, Hkv, G, HW, list_len;
 };
 
-// Work items are (merge-list entry {b, q, first slot, pieces}, query head of
-// the segment); workgroups stride over them.  A workgroup's 256 threads are
-// 32 float4 chunks of head_dim times kCombineLanes piece lanes: lane l merges
-// pieces l, l + kCombineLanes, ... (running log-sum-exp, kCombineUnroll loads
-// in flight), then the lanes' (max, normaliser, accumulator) are merged in
-// LDS.  Empty requests get zeros.
+// The merge list holds {b, q, first slot, pieces} per segment to merge.
+// Work items, strided over the workgroups:
+//   short entries (<= kShortMerge pieces, incl. 0 for empty requests): one
+//     item per segment; its HW * G query heads x 32 float4 chunks of head_dim
+//     are spread over the threads, each merging all pieces of its chunk with
+//     the loads of a block of pieces issued before use;
+//   long entries: one item per (segment, query head); 32 chunks x
+//     kCombineLanes piece lanes, lane l merging pieces l, l + lanes, ..., then
+//     the lanes' (max, normaliser, accumulator) merged in LDS.
+// Merging is a running log-sum-exp in the exp2 domain.
 constexpr int kCombineLanes = kCombineThreads / (kHeadDim / 4);
 constexpr int kCombineUnroll = 4;
+
+struct Lse {
+    float m, l;
+    f32x4 o;
+};
+
+// Merge pieces p0, p0 + step, ... (< n) of one (slot row, chunk) into r.
+__device__ inline void lse_pieces(const CombineArgs &a, Lse &r, int first, int n, int p0, int step,
+                                  int hi, int hh, int c4)
+{
+    for (; p0 < n; p0 += step * kCombineUnroll) {
+        float2 ml[kCombineUnroll];
+        f32x4 v[kCombineUnroll];
+#pragma unroll
+        for (int k = 0; k < kCombineUnroll; ++k) {
+            const int p = min(p0 + k * step, n - 1);
+            const size_t it = ((size_t)(first + p) * a.HW + hi) * a.G + hh;
+            ml[k] = a.part_ml[it];
+            v[k] = *(const f32x4 *)(a.part_acc + it * kHeadDim + 4 * c4);
+        }
+        float Mb = r.m;
+#pragma unroll
+        for (int k = 0; k < kCombineUnroll; ++k)
+            if (p0 + k * step < n)
+                Mb = fmaxf(Mb, ml[k].x);
+        const float sc = __builtin_amdgcn_exp2f(r.m - Mb);
+        r.l *= sc;
+        r.o *= sc;
+#pragma unroll
+        for (int k = 0; k < kCombineUnroll; ++k) {
+            if (p0 + k * step < n) {
+                const float w = __builtin_amdgcn_exp2f(ml[k].x - Mb);
+                r.l += w * ml[k].y;
+                r.o += w * v[k];
+            }
+        }
+        r.m = Mb;
+    }
+}
+
+template <int MODE>
+__device__ inline void store_out(const CombineArgs &a, size_t dst, f32x4 o)
+{
+    if constexpr (MODE == MODE_F32) {
+        *(f32x4 *)((float *)a.out + dst) = o;
+    } else {
+        *(u32x2 *)((uint16_t *)a.out + dst) =
+            u32x2{(unsigned)bf16_bits(o[0]) | ((unsigned)bf16_bits(o[1]) << 16),
+                  (unsigned)bf16_bits(o[2]) | ((unsigned)bf16_bits(o[3]) << 16)};
+    }
+}
 
 template <int MODE>
 __global__ void __launch_bounds__(kCombineThreads)
@@ -653,79 +718,114 @@ combine_kernel(const CombineArgs a)
     __shared__ float s_m[kCombineLanes][kHeadDim / 4];
     __shared__ float s_l[kCombineLanes][kHeadDim / 4];
     __shared__ f32x4 s_o[kCombineLanes][kHeadDim / 4];
-    const int n_merge = a.hdr->n_merge;
+    const int n_short = a.hdr->n_short, n_long = a.hdr->n_long;
     const int G = a.G, HW = a.HW;
     const int rows = HW * G;
-    const int c4 = threadIdx.x & (kHeadDim / 4 - 1);
-    const int pl = threadIdx.x / (kHeadDim / 4);
-    for (int item = blockIdx.x; item < n_merge * rows; item += gridDim.x) {
-        const int e = item / rows, row = item - (item / rows) * rows;
-        const int4 m = a.merge[e];
-        const int b = m.x, q = m.y, first = m.z, n = m.w;
-        const int hi = row / G, hh = row - hi * G;
-        float M = -INFINITY, den = 0.f;
-        f32x4 o = {0.f, 0.f, 0.f, 0.f};
-        for (int p0 = pl; p0 < n; p0 += kCombineLanes * kCombineUnroll) {
-            float2 ml[kCombineUnroll];
-            f32x4 v[kCombineUnroll];
-#pragma unroll
-            for (int k = 0; k < kCombineUnroll; ++k) {
-                const int p = min(p0 + k * kCombineLanes, n - 1);
-                const size_t it = ((size_t)(first + p) * HW + hi) * G + hh;
-                ml[k] = a.part_ml[it];
-                v[k] = *(const f32x4 *)(a.part_acc + it * kHeadDim + 4 * c4);
+    const int n_items = n_short + n_long * rows;
+    for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+        if (item < n_short) {
+            const int4 m = a.merge[item];
+            const int b = m.x, q = m.y, first = m.z, n = m.w;
+            for (int u = threadIdx.x; u < rows * (kHeadDim / 4); u += kCombineThreads) {
+                const int row = u / (kHeadDim / 4), c4 = u - row * (kHeadDim / 4);
+                const int hi = row / G, hh = row - hi * G;
+                Lse r = {-INFINITY, 0.f, {0.f, 0.f, 0.f, 0.f}};
+                lse_pieces(a, r, first, n, 0, 1, hi, hh, c4);
+                const f32x4 o = n > 0 ? r.o * (1.0f / r.l) : r.o;
+                store_out<MODE>(a, ((size_t)b * a.Hq + (q * HW + hi) * G + hh) * kHeadDim + 4 * c4, o);
             }
-            float Mb = M;
-#pragma unroll
-            for (int k = 0; k < kCombineUnroll; ++k)
-                if (p0 + k * kCombineLanes < n)
-                    Mb = fmaxf(Mb, ml[k].x);
-            const float r = __builtin_amdgcn_exp2f(M - Mb);
-            den *= r;
-            o *= r;
-#pragma unroll
-            for (int k = 0; k < kCombineUnroll; ++k) {
-                if (p0 + k * kCombineLanes < n) {
-                    const float w = __builtin_amdgcn_exp2f(ml[k].x - Mb);
-                    den += w * ml[k].y;
-                    o += w * v[k];
-                }
-            }
-            M = Mb;
-        }
-        s_m[pl][c4] = M;
-        s_l[pl][c4] = den;
-        s_o[pl][c4] = o;
-        __syncthreads();
-        if (pl == 0) {
-            f32x4 res = {0.f, 0.f, 0.f, 0.f};
-            if (n > 1) {
+        } else {
+            const int e = (item - n_short) / rows, row = (item - n_short) - e * rows;
+            const int4 m = a.merge[a.list_len - 1 - e];
+            const int b = m.x, q = m.y, first = m.z, n = m.w;
+            const int hi = row / G, hh = row - hi * G;
+            const int c4 = threadIdx.x & (kHeadDim / 4 - 1);
+            const int pl = threadIdx.x / (kHeadDim / 4);
+            Lse r = {-INFINITY, 0.f, {0.f, 0.f, 0.f, 0.f}};
+            lse_pieces(a, r, first, n, pl, kCombineLanes, hi, hh, c4);
+            s_m[pl][c4] = r.m;
+            s_l[pl][c4] = r.l;
+            s_o[pl][c4] = r.o;
+            __syncthreads();
+            if (pl == 0) {
+                // every lane holds at least one piece (n > kShortMerge >= lanes)
                 float Mt = -INFINITY;
 #pragma unroll
                 for (int x = 0; x < kCombineLanes; ++x)
                     Mt = fmaxf(Mt, s_m[x][c4]);
-                float dt = 0.f;
+                float lt = 0.f;
+                f32x4 o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int x = 0; x < kCombineLanes; ++x) {
-                    if (x < n) {   // lanes without pieces hold M = -inf
-                        const float w = __builtin_amdgcn_exp2f(s_m[x][c4] - Mt);
-                        dt += w * s_l[x][c4];
-                        res += w * s_o[x][c4];
-                    }
+                    const float w = __builtin_amdgcn_exp2f(s_m[x][c4] - Mt);
+                    lt += w * s_l[x][c4];
+                    o += w * s_o[x][c4];
                 }
-                res *= 1.0f / dt;
+                store_out<MODE>(a, ((size_t)b * a.Hq + (q * HW + hi) * G + hh) * kHeadDim + 4 * c4,
+                                o * (1.0f / lt));
             }
-            const size_t dst = ((size_t)b * a.Hq + (q * HW + hi) * G + hh) * kHeadDim + 4 * c4;
-            if constexpr (MODE == MODE_F32) {
-                *(f32x4 *)((float *)a.out + dst) = res;
-            } else {
-                *(u32x2 *)((uint16_t *)a.out + dst) =
-                    u32x2{(unsigned)bf16_bits(res[0]) | ((unsigned)bf16_bits(res[1]) << 16),
-                          (unsigned)bf16_bits(res[2]) | ((unsigned)bf16_bits(res[3]) << 16)};
-            }
+            __syncthreads();
         }
-        __syncthreads();
     }
+}
+
+// ---------------------------------------------------------------- KV append
+// The step before attention in a decode iteration: each request's new K and
+// V rows (n_kv_heads * head_dim bf16, contiguous in the token-major page) go
+// to slot pos mod 16 of page page_table[b][pos / 16].  One wave per request,
+// 16-byte loads and stores.
+constexpr int kAppendThreads = 64;
+
+__global__ void __launch_bounds__(kAppendThreads)
+kv_append_kernel(const u32x4 *__restrict__ k_new, const u32x4 *__restrict__ v_new,
+                 u32x4 *__restrict__ k_pages, u32x4 *__restrict__ v_pages,
+                 const int32_t *__restrict__ page_table, const int32_t *__restrict__ positions,
+                 int Hkv, int maxp)
+{
+    const int b = blockIdx.x;
+    const int pos = positions[b];
+    if (pos < 0 || pos >= maxp * kPage)
+        return;
+    const int pg = page_table[(size_t)b * maxp + pos / kPage];
+    const int chunks = Hkv * kHeadDim / 8;          // 16-byte chunks per token row
+    const size_t dst = ((size_t)pg * kPage + pos % kPage) * chunks;
+    const size_t src = (size_t)b * chunks;
+    for (int c = threadIdx.x; c < chunks; c += kAppendThreads) {
+        k_pages[dst + c] = k_new[src + c];
+        v_pages[dst + c] = v_new[src + c];
+    }
+}
+
+// ---------------------------------------------------------------- HBM read ceiling
+// Measurement aid: every thread streams 16-byte non-temporal loads, 16 in
+// flight, grid-stride over the buffer, and folds them into one word that is
+// stored only if it equals a value no real data produces in practice (so the
+// loads cannot be dropped).  Gives the read rate the attention kernel is
+// measured against.
+constexpr int kStreamThreads = 256;
+constexpr int kStreamUnroll = 16;
+
+__global__ void __launch_bounds__(kStreamThreads)
+stream_read_kernel(const u32x4 *__restrict__ p, size_t n16, unsigned *__restrict__ sink)
+{
+    const size_t stride = (size_t)gridDim.x * kStreamThreads;
+    size_t i = (size_t)blockIdx.x * kStreamThreads + threadIdx.x;
+    unsigned acc = 0;
+    for (; i + (kStreamUnroll - 1) * stride < n16; i += kStreamUnroll * stride) {
+        u32x4 v[kStreamUnroll];
+#pragma unroll
+        for (int u = 0; u < kStreamUnroll; ++u)
+            v[u] = __builtin_nontemporal_load(p + i + u * stride);
+#pragma unroll
+        for (int u = 0; u < kStreamUnroll; ++u)
+            acc ^= v[u][0] ^ v[u][1] ^ v[u][2] ^ v[u][3];
+    }
+    for (; i < n16; i += stride) {
+        const u32x4 v = p[i];
+        acc ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+    }
+    if (acc == 0x9E3779B9u)
+        *sink = acc;
 }
 
 // ---------------------------------------------------------------- host side
@@ -984,6 +1084,7 @@ int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, in
     c.Hkv = n_kv_heads;
     c.G = G;
     c.HW = heads_per_group(n_kv_heads);
+    c.list_len = num_seqs * (n_kv_heads / c.HW);
     int cus = 0;
     st = num_cus(&cus);
     if (st)
@@ -1054,6 +1155,39 @@ int vd_decode_gather(const void *k_pages, const void *v_pages, const int32_t *pa
     a.out = k_out;
     a.out2 = v_out;
     return enqueue_attn(a, 1, MODE_GATHER, stream);
+}
+
+int vd_kv_append(const void *k_new, const void *v_new, void *k_pages, void *v_pages,
+                 const int32_t *page_table, const int32_t *positions, int num_seqs,
+                 int n_kv_heads, int head_dim, int page_size, int max_pages_per_seq,
+                 hipStream_t stream)
+{
+    int st = check_shapes(num_seqs, n_kv_heads, n_kv_heads, head_dim, page_size,
+                          max_pages_per_seq, 0);
+    if (st)
+        return st;
+    if (!k_new || !v_new || !k_pages || !v_pages || !page_table || !positions)
+        return VD_ERROR_INVALID_VALUE;
+    if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_pages, 16) ||
+        !aligned(v_pages, 16) || !aligned(page_table, 4) || !aligned(positions, 4))
+        return VD_ERROR_INVALID_VALUE;
+    if (num_seqs == 0)
+        return VD_SUCCESS;
+    hipLaunchKernelGGL(kv_append_kernel, dim3(num_seqs), dim3(kAppendThreads), 0, stream,
+                       (const u32x4 *)k_new, (const u32x4 *)v_new, (u32x4 *)k_pages,
+                       (u32x4 *)v_pages, page_table, positions, n_kv_heads, max_pages_per_seq);
+    return launch_status();
+}
+
+int vd_stream_read(const void *buf, size_t bytes, void *sink, int blocks, hipStream_t stream)
+{
+    if (!buf || !sink || blocks <= 0 || !aligned(buf, 16) || !aligned(sink, 4) || bytes % 16 != 0)
+        return VD_ERROR_INVALID_VALUE;
+    if (bytes == 0)
+        return VD_SUCCESS;
+    hipLaunchKernelGGL(stream_read_kernel, dim3(blocks), dim3(kStreamThreads), 0, stream,
+                       (const u32x4 *)buf, bytes / 16, (unsigned *)sink);
+    return launch_status();
 }
 
 }  // extern "C"

@@ -260,6 +260,32 @@ def pin_gather(orc):
     assert np.array_equal(vo, np.stack([c["v"][p, s] for p, s in rows]))
 
 
+# ---------------------------------------------------------------- KV append
+def pin_kv_append(orc):
+    """After appending token pos of request b, the request's row pos is the
+    new row (direct indexing of the pools) and no other byte changed;
+    negative and out-of-table positions write nothing."""
+    c = case([16, 1, 33, 0, 5], hq=4, hkv=2, seed=16, pt_stride=4)
+    rng = np.random.default_rng(5)
+    k_new = rng.integers(0, 1 << 16, (5, 2, 128), dtype=np.uint16)
+    v_new = rng.integers(0, 1 << 16, (5, 2, 128), dtype=np.uint16)
+    # request 1: position 64 is past its 4-entry table row (a missing bound
+    # would read row 2's first entry, still inside the table); request 3: -1
+    pos = np.array([15, 64, 33, -1, 4], dtype=np.int32)
+    k, v = c["k"].copy(), c["v"].copy()
+    orc.kv_append(k_new, v_new, k, v, c["pt"], pos)
+    ek, ev = c["k"].copy(), c["v"].copy()
+    for b, p in enumerate(pos):
+        if 0 <= p < c["pt"].shape[1] * 16:
+            ek[c["pt"][b, p // 16], p % 16] = k_new[b]
+            ev[c["pt"][b, p // 16], p % 16] = v_new[b]
+    assert np.array_equal(k, ek) and np.array_equal(v, ev), "kv append"
+    L = np.array([16, 1, 34, 0, 5], dtype=np.int32)
+    ko, vo = orc.gather(k, v, c["pt"], L)
+    assert np.array_equal(ko[15], k_new[0]) and np.array_equal(vo[15], v_new[0])
+    assert np.array_equal(ko[16 + 1 + 33], k_new[2]) and np.array_equal(vo[16 + 1 + 34 + 4], v_new[4])
+
+
 ALL_PINS = [pin_brute_force, pin_single_token, pin_constant_v, pin_shift_invariance,
             pin_page_permutation, pin_closed_forms, pin_gqa_equals_duplicated_mha,
-            pin_one_hot, pin_torch_sdpa, pin_edges, pin_gather]
+            pin_one_hot, pin_torch_sdpa, pin_edges, pin_gather, pin_kv_append]

@@ -116,6 +116,17 @@ def test_plan_combine_gather_argument_errors():
                               None) == vd.VD_ERROR_NOT_SUPPORTED
 
 
+def test_append_and_stream_argument_errors():
+    L = vd.lib()
+    assert L.vd_kv_append(None, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 8, 128, 16, 63, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_kv_append(FAKE, FAKE, MIS, FAKE, FAKE, FAKE, 4, 8, 128, 16, 63, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_kv_append(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 8, 64, 16, 63, None) == vd.VD_ERROR_NOT_SUPPORTED
+    assert L.vd_kv_append(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, -1, 8, 128, 16, 63, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_stream_read(None, 1024, FAKE, 8, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_stream_read(FAKE, 1000, FAKE, 8, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_stream_read(FAKE, 1024, FAKE, 0, None) == vd.VD_ERROR_INVALID_VALUE
+
+
 def test_product_does_not_reference_oracle():
     """The product package neither imports nor links the oracle."""
     pkg = os.path.join(ROOT, "paper_2509_04827_amd")

@@ -300,6 +300,47 @@ def test_staged_plan_once_two_layers():
     assert torch.equal(outs[0].view(torch.int32).cpu(), fused.view(torch.int32).cpu())
 
 
+# ------------------------------------------------------------------ KV append
+def test_kv_append_bit_exact():
+    say("case: KV append")
+    c = custom([16, 1, 33, 0, 5, 100, 257, 15], seed=30, pt_stride=20)
+    B = c["num_seqs"]
+    positions = torch.tensor([15, 1, 33, -1, 4, 100, 320, 319], dtype=torch.int32)
+    g = torch.Generator().manual_seed(31)
+    k_new = torch.randn((B, 8, 128), generator=g).to(torch.bfloat16)
+    v_new = torch.randn((B, 8, 128), generator=g).to(torch.bfloat16)
+    d = dev_case(c)
+    vd.vd_kv_append(k_new.to(DEV), v_new.to(DEV), d["k_pages"], d["v_pages"], d["page_table"],
+                    positions.to(DEV))
+    torch.cuda.synchronize()
+    hk, hv = bits(c["k_pages"]).copy(), bits(c["v_pages"]).copy()
+    oracle.kv_append(bits(k_new), bits(v_new), hk, hv, c["page_table"].numpy(), positions.numpy())
+    assert np.array_equal(bits(d["k_pages"].cpu()), hk)
+    assert np.array_equal(bits(d["v_pages"].cpu()), hv)
+
+
+def test_decode_step_append_then_attend():
+    """One decode iteration: append each request's newest K/V at position L_b,
+    then attend over L_b + 1 tokens."""
+    say("case: append then attend")
+    lens = [15, 16, 1, 300, 4095, 17]
+    c = custom([x + 1 for x in lens], seed=32)        # pages for the new token exist
+    B = len(lens)
+    pos = torch.tensor(lens, dtype=torch.int32)
+    g = torch.Generator().manual_seed(33)
+    k_new = torch.randn((B, 8, 128), generator=g).to(torch.bfloat16)
+    v_new = torch.randn((B, 8, 128), generator=g).to(torch.bfloat16)
+    d = dev_case(c)
+    vd.vd_kv_append(k_new.to(DEV), v_new.to(DEV), d["k_pages"], d["v_pages"], d["page_table"],
+                    pos.to(DEV))
+    got = run_gpu(d)
+    hk, hv = bits(c["k_pages"]).copy(), bits(c["v_pages"]).copy()
+    oracle.kv_append(bits(k_new), bits(v_new), hk, hv, c["page_table"].numpy(), pos.numpy())
+    ref = oracle.decode_attn(bits(c["q"]), hk, hv, c["page_table"].numpy(),
+                             c["seq_lens"].numpy(), c["scale"])
+    check_f32(got, ref, "append then attend")
+
+
 def test_device_errors_leave_stream_clean():
     say("case: error codes on device")
     c = custom([10], seed=19)

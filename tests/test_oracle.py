@@ -35,6 +35,10 @@ MUTANTS = {
                            "for (int t = 0; t < L - 1; ++t) {\n        const int32_t p = page_table[(size_t)b * max_pages_per_seq + t / page_size];\n        const uint16_t *vt"),
     "bf16_widen_shift": ("uint32_t bits = (uint32_t)h << 16;", "uint32_t bits = (uint32_t)h << 15;"),
     "gather_v_from_k": ("memcpy(v_out + dst, v_pages + src", "memcpy(v_out + dst, k_pages + src"),
+    "append_slot": ("(size_t)(pos % page_size) * row;\n        memcpy(k_pages",
+                    "(size_t)((pos + 1) % page_size) * row;\n        memcpy(k_pages"),
+    "append_no_skip": ("if (pos < 0 || pos >= max_pages_per_seq * page_size)\n            continue;",
+                       "if (pos < 0)\n            continue;"),
 }
 
 
@@ -58,7 +62,7 @@ class _MutantOracle:
         self._lib = ctypes.CDLL(libpath)
         proto = oracle._load()
         for fn in ("vdo_decode_attn_f64", "vdo_decode_attn_rows_f64", "vdo_gather",
-                   "vdo_softmax_f64", "vdo_max_threads"):
+                   "vdo_kv_append", "vdo_softmax_f64", "vdo_max_threads"):
             getattr(self._lib, fn).argtypes = getattr(proto, fn).argtypes
             getattr(self._lib, fn).restype = getattr(proto, fn).restype
 
