@@ -57,6 +57,8 @@ def _load():
         lib.vdo_gather.restype = I
         lib.vdo_kv_append.argtypes = [P, P, P, P, P, P, I, I, I, I, I]
         lib.vdo_kv_append.restype = I
+        lib.vdo_gemm_f64.argtypes = [P, P, P, I, I, I, I]
+        lib.vdo_gemm_f64.restype = I
         lib.vdo_softmax_f64.argtypes = [P, I, P]
         lib.vdo_softmax_f64.restype = None
         lib.vdo_max_threads.argtypes = []
@@ -159,6 +161,19 @@ def kv_append(k_new, v_new, k_pages, v_pages, page_table, positions) -> None:
                                page_table.shape[1])
     if rc != 0:
         raise RuntimeError("oracle vdo_kv_append failed with code %d" % rc)
+
+
+def gemm(x, w, nthreads: int = 0) -> np.ndarray:
+    """y float64 [M][N] = x [M][K] . w [N][K]^T for bf16 bit patterns (uint16)."""
+    x, w = _u16(x), _u16(w)
+    M, K = x.shape
+    N, K2 = w.shape
+    assert K2 == K
+    y = np.zeros((M, N), dtype=np.float64)
+    rc = _load().vdo_gemm_f64(_ptr(x), _ptr(w), _ptr(y), M, N, K, int(nthreads))
+    if rc != 0:
+        raise RuntimeError("oracle vdo_gemm_f64 failed with code %d" % rc)
+    return y
 
 
 def softmax(s) -> np.ndarray:

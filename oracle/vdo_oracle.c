@@ -246,6 +246,33 @@ int vdo_kv_append(const uint16_t *k_new, const uint16_t *v_new, uint16_t *k_page
     return 0;
 }
 
+/*
+ * Dense projection of a decode step: y[m][n] = sum_k x[m][k] * w[n][k] for
+ * x uint16 (bf16) [M][K] and w uint16 (bf16) [N][K] (the layout of a linear
+ * layer's weight), y double [M][N]; plain ascending fp64 sums.  The paper's
+ * decode latency model charges these GEMMs to N_req (Sec. 5.4, Eq.
+ * pred-itl) and ties their latency steps to tile quantisation (Sec. 3.3).
+ */
+int vdo_gemm_f64(const uint16_t *x, const uint16_t *w, double *y, int M, int N, int K,
+                 int nthreads)
+{
+    if (M < 0 || N < 0 || K < 0)
+        return 1;
+#ifdef _OPENMP
+    if (nthreads <= 0)
+        nthreads = omp_get_max_threads();
+#pragma omp parallel for schedule(static) num_threads(nthreads)
+#endif
+    for (long i = 0; i < (long)M * N; ++i) {
+        const int m = (int)(i / N), n = (int)(i % N);
+        double acc = 0.0;
+        for (int k = 0; k < K; ++k)
+            acc += vdo_bf16_to_f64(x[(size_t)m * K + k]) * vdo_bf16_to_f64(w[(size_t)n * K + k]);
+        y[i] = acc;
+    }
+    return 0;
+}
+
 /* Max-subtracted softmax of n scores (exposed so tests can pin it alone). */
 void vdo_softmax_f64(const double *s, int n, double *w)
 {

@@ -286,6 +286,29 @@ def pin_kv_append(orc):
     assert np.array_equal(ko[16 + 1 + 33], k_new[2]) and np.array_equal(vo[16 + 1 + 34 + 4], v_new[4])
 
 
+# ---------------------------------------------------------------- GEMM
+def pin_gemm(orc):
+    """Brute force with exactly rounded sums; an identity weight returns x;
+    float64 matmul of a library agrees."""
+    rng = np.random.default_rng(7)
+    x = (rng.standard_normal((3, 40)).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    w = (rng.standard_normal((5, 40)).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    y = orc.gemm(x, w)
+    for m in range(3):
+        for n in range(5):
+            ref = math.fsum(f_of(a) * f_of(b) for a, b in zip(x[m], w[n]))
+            assert abs(y[m, n] - ref) <= 1e-12, ("gemm brute force", m, n)
+    eye = np.zeros((40, 40), dtype=np.uint16)
+    eye[np.arange(40), np.arange(40)] = bf16_bits(1.0)
+    xf = np.array([[f_of(a) for a in row] for row in x])
+    assert np.array_equal(orc.gemm(x, eye), xf), "gemm identity"
+    xl = (rng.standard_normal((7, 300)).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    wl = (rng.standard_normal((33, 300)).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    tx = torch.from_numpy(xl.astype(np.uint32) << 16).view(torch.float32).double()
+    tw = torch.from_numpy(wl.astype(np.uint32) << 16).view(torch.float32).double()
+    assert np.abs(orc.gemm(xl, wl) - (tx @ tw.T).numpy()).max() <= 1e-10, "gemm vs library"
+
+
 ALL_PINS = [pin_brute_force, pin_single_token, pin_constant_v, pin_shift_invariance,
             pin_page_permutation, pin_closed_forms, pin_gqa_equals_duplicated_mha,
-            pin_one_hot, pin_torch_sdpa, pin_edges, pin_gather, pin_kv_append]
+            pin_one_hot, pin_torch_sdpa, pin_edges, pin_gather, pin_kv_append, pin_gemm]

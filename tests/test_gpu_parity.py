@@ -300,6 +300,32 @@ def test_staged_plan_once_two_layers():
     assert torch.equal(outs[0].view(torch.int32).cpu(), fused.view(torch.int32).cpu())
 
 
+# ------------------------------------------------------------------ randomized sweep
+@pytest.mark.parametrize("trial", range(12))
+def test_random_shapes(trial):
+    """Seeded random shapes: request count, GQA ratio, KV heads, a length mix
+    with empty, one-token, page-boundary and long requests, table stride and
+    range size."""
+    rng = np.random.default_rng(1000 + trial)
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 4, 8, 16]))
+    B = int(rng.integers(1, 40))
+    pool = [0, 1, 15, 16, 17, 31, 33, 255, 256, 257] + list(rng.integers(1, 3000, 8))
+    lengths = [int(rng.choice(pool)) for _ in range(B)]
+    if rng.random() < 0.3:
+        lengths[int(rng.integers(0, B))] = int(rng.integers(8000, 40000))
+    maxp = max(1, max((x + 15) // 16 for x in lengths))
+    stride = maxp + int(rng.integers(0, 5))
+    flags = vd.VD_FLAG_RANGE_TILES(int(rng.integers(1, 256))) if rng.random() < 0.4 else 0
+    say("case: random trial %d B %d G %d Hkv %d flags %#x lengths %s"
+        % (trial, B, G, hkv, flags, lengths))
+    c = custom(lengths, hq=G * hkv, hkv=hkv, seed=2000 + trial, pt_stride=stride)
+    d = dev_case(c)
+    ref = ref_of(c)
+    check_f32(run_gpu(d, flags=flags), ref, "random %d" % trial)
+    check_bf16(run_gpu(d, torch.bfloat16, flags=flags), ref, "random %d" % trial)
+
+
 # ------------------------------------------------------------------ KV append
 def test_kv_append_bit_exact():
     say("case: KV append")

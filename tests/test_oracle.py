@@ -37,6 +37,8 @@ MUTANTS = {
     "gather_v_from_k": ("memcpy(v_out + dst, v_pages + src", "memcpy(v_out + dst, k_pages + src"),
     "append_slot": ("(size_t)(pos % page_size) * row;\n        memcpy(k_pages",
                     "(size_t)((pos + 1) % page_size) * row;\n        memcpy(k_pages"),
+    "gemm_transposed_w": ("vdo_bf16_to_f64(w[(size_t)n * K + k]);", "vdo_bf16_to_f64(w[(size_t)k * N + n]);"),
+    "gemm_k_off_by_one": ("for (int k = 0; k < K; ++k)\n            acc +=", "for (int k = 1; k < K; ++k)\n            acc +="),
     "append_no_skip": ("if (pos < 0 || pos >= max_pages_per_seq * page_size)\n            continue;",
                        "if (pos < 0)\n            continue;"),
 }
@@ -62,7 +64,7 @@ class _MutantOracle:
         self._lib = ctypes.CDLL(libpath)
         proto = oracle._load()
         for fn in ("vdo_decode_attn_f64", "vdo_decode_attn_rows_f64", "vdo_gather",
-                   "vdo_kv_append", "vdo_softmax_f64", "vdo_max_threads"):
+                   "vdo_kv_append", "vdo_gemm_f64", "vdo_softmax_f64", "vdo_max_threads"):
             getattr(self._lib, fn).argtypes = getattr(proto, fn).argtypes
             getattr(self._lib, fn).restype = getattr(proto, fn).restype
 
