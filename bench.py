@@ -166,6 +166,71 @@ def latency_surface(outdir: str, iters: int = 10, warmup: int = 3):
     print(json.dumps({"surface_points": len(rows), "fit": fit}), flush=True)
 
 
+GEMM_SHAPES = (("qkv", 6144, 4096), ("o_proj", 4096, 4096), ("gate_up", 28672, 4096),
+               ("down", 4096, 14336))
+GEMM_M = (1, 2, 4, 8, 16, 24, 32, 48, 64, 96, 128, 160, 192, 224, 240, 248, 255, 256, 257, 264,
+          272, 288, 320, 384, 448, 512, 513, 640, 768, 1024)
+
+
+def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
+    """Decode-step projection GEMMs of a Llama-3-8B-shaped layer (hidden 4096,
+    KV 8 x 128, MLP 14336) over the decode batch M: this library's
+    weight-streaming kernel (M <= 64) against torch.matmul (hipBLASLt), to
+    locate the batch steps the paper traces to tile quantisation (Sec. 3.3)."""
+    import numpy as np
+    import torch
+
+    import paper_2509_04827_amd as vd
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    gen = torch.Generator(device=dev).manual_seed(0)
+    stream = torch.cuda.current_stream()
+    rows = []
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(iters):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / iters
+
+    for name, N, K in GEMM_SHAPES:
+        w = torch.randn((N, K), generator=gen, device=dev).to(torch.bfloat16)
+        for M in GEMM_M:
+            x = torch.randn((M, K), generator=gen, device=dev).to(torch.bfloat16)
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            us_lib = timed(lambda: torch.matmul(x, w.t(), out=y))
+            us_own = None
+            if M <= 64:
+                ws = torch.empty(max(16, vd.vd_gemm_workspace_size(M, N, K)), dtype=torch.uint8,
+                                 device=dev)
+                us_own = timed(lambda: vd.vd_gemm_bf16(x, w, y, ws, stream=stream))
+            nbytes = (N * K + M * K + M * N) * 2
+            flops = 2.0 * M * N * K
+            floor_us = max(nbytes / (PEAK_HBM_GBS * 1e3), flops / 2.5e9)
+            rows.append(dict(shape=name, M=M, N=N, K=K, us_hipblaslt=round(us_lib, 2),
+                             us_own=None if us_own is None else round(us_own, 2),
+                             roofline_us=round(floor_us, 2),
+                             gbs_hipblaslt=round(nbytes / us_lib / 1e3, 1),
+                             gbs_own=None if us_own is None else round(nbytes / us_own / 1e3, 1)))
+            print("gemm %-8s M %5d N %6d K %6d  hipBLASLt %8.2f us  own %8s us  roofline %6.2f us"
+                  % (name, M, N, K, us_lib, "-" if us_own is None else "%.2f" % us_own, floor_us),
+                  file=sys.stderr, flush=True)
+    os.makedirs(outdir, exist_ok=True)
+    keys = list(rows[0].keys())
+    with open(os.path.join(outdir, "decode_gemm_sweep.csv"), "w") as f:
+        f.write(",".join(keys) + "\n")
+        for r in rows:
+            f.write(",".join("" if r[k] is None else str(r[k]) for k in keys) + "\n")
+    print(json.dumps({"gemm_points": len(rows)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -180,6 +245,9 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after timing, copy a BYTES-sized buffer 3 times (a plain copy "
                          "kernel of known size, to scale HBM counters by)")
+    ap.add_argument("--gemm-sweep", metavar="DIR", default=None,
+                    help="instead of the bench line, time the decode-step projection GEMMs "
+                         "over the batch size and write DIR/decode_gemm_sweep.csv")
     ap.add_argument("--surface", metavar="DIR", default=None,
                     help="instead of the bench line, measure the latency surface over "
                          "(batch, tokens per request) and write DIR/decode_latency_surface.{csv,md}")
@@ -200,6 +268,9 @@ def main():
 
     if args.surface:
         latency_surface(args.surface)
+        return
+    if args.gemm_sweep:
+        gemm_sweep(args.gemm_sweep)
         return
 
     w = WORKLOADS[args.workload]

@@ -173,6 +173,23 @@ int vd_kv_append(const void *k_new, const void *v_new, void *k_pages,
                  hipStream_t stream);
 
 /*
+ * Decode-step projection: y[m][n] = sum_k x[m][k] * w[n][k] for the N_req
+ * rows of a decode iteration (the GEMM work the paper's decode latency model
+ * charges to N_req, Sec. 5.4, Eq. pred-itl; its batch steps, Sec. 3.3).
+ *   x  bf16 [M][K], row-major           w  bf16 [N][K] (a linear layer's weight)
+ *   y  bf16 (RNE) or fp32 with VD_FLAG_OUT_F32, [M][N]
+ * fp32 accumulation; the result does not depend on the device (fixed
+ * reduction order).  Supported: 1 <= M <= 64, N a multiple of 64, K a
+ * multiple of 512.  x, w, y, workspace 16-byte aligned.  The workspace
+ * (vd_gemm_workspace_size) holds fp32 partials when K is split across
+ * workgroups; it may be NULL when that size is 0.  Errors as above.
+ */
+size_t vd_gemm_workspace_size(int M, int N, int K, unsigned flags);
+int vd_gemm_bf16(const void *x, const void *w, void *y, int M, int N, int K,
+                 void *workspace, size_t workspace_bytes, unsigned flags,
+                 hipStream_t stream);
+
+/*
  * Measurement aid, not part of the attention path: reads `bytes` (a multiple
  * of 16) from device buffer `buf` with 16-byte non-temporal loads from
  * `blocks` workgroups of 256 threads, and may write 4 bytes to device pointer

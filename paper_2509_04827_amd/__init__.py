@@ -36,7 +36,8 @@ VD_FLAG_OUT_F32 = 1 << 0
 VD_FLAG_RANGE_SHIFT = 8
 
 EXPORTS = ("vd_status_string", "vd_decode_workspace_size", "vd_decode_attn", "vd_decode_plan",
-           "vd_decode_partial", "vd_decode_combine", "vd_decode_gather", "vd_kv_append", "vd_stream_read")
+           "vd_decode_partial", "vd_decode_combine", "vd_decode_gather", "vd_kv_append", "vd_gemm_workspace_size", "vd_gemm_bf16",
+           "vd_stream_read")
 
 
 def VD_FLAG_RANGE_TILES(n: int) -> int:
@@ -73,7 +74,8 @@ def lib() -> ctypes.CDLL:
         L.vd_decode_gather.argtypes = [P, P, P, P, P, P, I, I, I, I, I, P, Z, P]
         L.vd_stream_read.argtypes = [P, Z, P, I, P]
         for n in ("vd_decode_attn", "vd_decode_partial", "vd_decode_plan", "vd_decode_combine",
-                  "vd_decode_gather", "vd_kv_append", "vd_stream_read"):
+                  "vd_decode_gather", "vd_kv_append", "vd_gemm_workspace_size", "vd_gemm_bf16",
+           "vd_stream_read"):
             getattr(L, n).restype = I
         _lib = L
     return _lib
@@ -172,6 +174,19 @@ def vd_kv_append(k_new, v_new, k_pages, v_pages, page_table, positions, stream=N
     _check(lib().vd_kv_append(_ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages),
                               _ptr(page_table), _ptr(positions), positions.shape[0], Hkv, D, S,
                               page_table.shape[1], _stream(stream)), "vd_kv_append")
+
+
+def vd_gemm_workspace_size(M: int, N: int, K: int, flags: int = 0) -> int:
+    return int(lib().vd_gemm_workspace_size(M, N, K, flags))
+
+
+def vd_gemm_bf16(x, w, y, workspace=None, flags: int = 0, stream=None) -> None:
+    """y [M][N] = x [M][K] . w [N][K]^T (y fp32 sets VD_FLAG_OUT_F32)."""
+    M, K = x.shape
+    N = w.shape[0]
+    _check(lib().vd_gemm_bf16(_ptr(x), _ptr(w), _ptr(y), M, N, K, _ptr(workspace),
+                              0 if workspace is None else workspace.numel(),
+                              _out_flags(y, flags), _stream(stream)), "vd_gemm_bf16")
 
 
 def vd_stream_read(buf, sink, blocks: int = 8192, stream=None) -> None:

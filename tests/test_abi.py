@@ -127,6 +127,19 @@ def test_append_and_stream_argument_errors():
     assert L.vd_stream_read(FAKE, 1024, FAKE, 0, None) == vd.VD_ERROR_INVALID_VALUE
 
 
+def test_gemm_argument_errors():
+    L = vd.lib()
+    assert vd.vd_gemm_workspace_size(64, 4096, 4096) == 8 * 64 * 4096 * 4
+    assert vd.vd_gemm_workspace_size(65, 4096, 4096) == 0      # M > 64
+    assert vd.vd_gemm_workspace_size(8, 4128, 4096) == 0       # N % 64
+    assert vd.vd_gemm_workspace_size(8, 4096, 4000) == 0       # K % 512
+    assert L.vd_gemm_bf16(None, FAKE, FAKE, 4, 64, 512, FAKE, 1 << 20, 0, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_gemm_bf16(FAKE, MIS, FAKE, 4, 64, 512, FAKE, 1 << 20, 0, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_gemm_bf16(FAKE, FAKE, FAKE, 0, 64, 512, FAKE, 1 << 20, 0, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_gemm_bf16(FAKE, FAKE, FAKE, 4, 64, 512, FAKE, 1 << 20, 1 << 4, None) == vd.VD_ERROR_INVALID_VALUE
+    assert L.vd_gemm_bf16(FAKE, FAKE, FAKE, 99, 64, 512, FAKE, 1 << 20, 0, None) == vd.VD_ERROR_NOT_SUPPORTED
+
+
 def test_product_does_not_reference_oracle():
     """The product package neither imports nor links the oracle."""
     pkg = os.path.join(ROOT, "paper_2509_04827_amd")
