@@ -256,6 +256,26 @@ def test_gqa_ratios(G, hkv):
     check_bf16(run_gpu(d, torch.bfloat16), ref, "G=%d" % G)
 
 
+def test_max_requests():
+    """8192 requests (the supported maximum): every planner thread owns eight
+    requests; mixed tiny, empty and one long request."""
+    rng = np.random.default_rng(40)
+    lengths = [int(x) for x in rng.choice([0, 1, 2, 7, 16, 17, 40], 8192)]
+    lengths[4097] = 5000
+    say("case: 8192 requests, N_kv %d" % sum(lengths))
+    c = custom(lengths, hq=8, hkv=2, seed=41)
+    d = dev_case(c)
+    ref = ref_of(c)
+    check_f32(run_gpu(d), ref, "8192 requests")
+
+
+def test_sixteen_kv_heads():
+    say("case: 32:16 heads and 16:16 heads")
+    for hq, hkv in ((32, 16), (16, 16)):
+        c = custom([1, 100, 2049, 33], hq=hq, hkv=hkv, seed=42 + hq)
+        check_f32(run_gpu(dev_case(c)), ref_of(c), "Hq %d Hkv %d" % (hq, hkv))
+
+
 def test_empty_requests():
     say("case: empty requests")
     c = custom([0, 5, 0, 300, 0], seed=14)
