@@ -25,7 +25,8 @@
 //
 // Three kernels on the caller's stream:
 //   plan_kernel     one workgroup: tile offsets per request, range starts,
-//                   per-segment partial slots.
+//                   and the list of segments to merge (first partial slot,
+//                   number of pieces).
 //   attn_kernel     one workgroup per range (grid-stride over ranges), one
 //                   wave per KV head of the group.  Per page:
 //                     K rows are loaded straight into MFMA A operands (lane =
@@ -38,7 +39,8 @@
 //                     permutes into the A operand of
 //                     v_mfma_f32_16x16x16_bf16, whose B operand is P exactly
 //                     as the score MFMA left it (P split into bf16 hi + lo).
-//   combine_kernel  log-sum-exp merge of the partials per (request, q head).
+//   combine_kernel  log-sum-exp merge of each listed segment's partials
+//                   (zeros for requests without tokens).
 //
 // All arithmetic is fp32; bf16 is only the storage type of Q/K/V, the MFMA
 // operand type, and the optional output type.
@@ -56,15 +58,14 @@ namespace {
 constexpr int kHeadDim = 128;
 constexpr int kPage = 16;
 constexpr int kMaxSeqs = 8192;         // planner keeps tile offsets in LDS
-constexpr int kMaxRangeTiles = 256;    // four 64-entry page-id windows per piece
+constexpr int kMaxRangeTiles = 512;    // eight 64-entry page-id windows per piece
 constexpr int kMinRangeTiles = 4;      // small steps: at least this many tiles per range
 constexpr int kMaxResidentGroups = 4096;
 constexpr int kPlanThreads = 1024;
 constexpr int kHeadsPerGroup = 4;      // preferred KV heads (waves) per attention workgroup
 constexpr int kAttnGroupsPerCU = 1;    // resident attention workgroups per CU
 constexpr int kPrefetch = 2;           // pages in flight per wave (ring of page tiles)
-constexpr int kMaxHeadsPerGroup = 8;
-constexpr int kAttnMaxThreads = 64 * kMaxHeadsPerGroup;
+constexpr int kAttnMaxThreads = 64 * kHeadsPerGroup;
 constexpr int kCombineThreads = 256;
 constexpr int kCombineGroupsPerCU = 4;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -89,8 +90,7 @@ struct PlanHeader {
 
 // ---------------------------------------------------------------- workspace
 struct WsLayout {
-    size_t hdr, tok_base, seg, merge, ranges, part_ml, part_acc, total;
-    long long cap_ranges, cap_slots;
+    size_t hdr, tok_base, merge, ranges, part_ml, part_acc, total;
 };
 
 __host__ __device__ inline long long ceil_div_ll(long long a, long long b) { return (a + b - 1) / b; }
@@ -123,14 +123,11 @@ inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced)
     size_t o = 0;
     l.hdr = o;       o = align_up(o + sizeof(PlanHeader), 256);
     l.tok_base = o;  o = align_up(o + sizeof(long long) * (size_t)(B + 1), 256);
-    l.seg = o;       o = align_up(o + sizeof(int2) * (size_t)B * (Hkv / HW), 256);
     l.merge = o;     o = align_up(o + sizeof(int4) * (size_t)B * (Hkv / HW), 256);
     l.ranges = o;    o = align_up(o + sizeof(int4) * (size_t)(cap + 1), 256);
     l.part_ml = o;   o = align_up(o + sizeof(float2) * (size_t)slots * G, 256);
     l.part_acc = o;  o = align_up(o + sizeof(float) * (size_t)slots * G * kHeadDim, 256);
     l.total = o;
-    l.cap_ranges = cap;
-    l.cap_slots = slots;
     return l;
 }
 
@@ -263,7 +260,6 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
     // other than exactly one piece (split, or empty request) go on the merge
     // list for the combine kernel: up to kShortMerge pieces from the front,
     // more from the back
-    int2 *seg = (int2 *)(ws + lay.seg);
     int4 *merge = (int4 *)(ws + lay.merge);
     for (int s = t; s < B * Hg; s += kPlanThreads) {
         const int b = s / Hg, q = s - (s / Hg) * Hg;
@@ -274,7 +270,6 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
             const int w0 = range_of(t0, T, W), w1 = range_of(t1, T, W);
             e = make_int2(w0 + s, w1 - w0 + 1);
         }
-        seg[s] = e;
         if (e.y != 1) {
             if (e.y <= kShortMerge)
                 merge[atomicAdd(&s_nshort, 1)] = make_int4(b, q, e.x, e.y);
