@@ -31,14 +31,21 @@
 //                   wave per KV head of the group.  Per page:
 //                     K rows are loaded straight into MFMA A operands (lane =
 //                     token row); scores = K Q^T with v_mfma_f32_16x16x32_bf16
-//                     against the group's G query heads (zero-padded to 16
-//                     columns);
+//                     against the group's G query heads (columns past G
+//                     repeat head G-1 and are never stored);
 //                     online softmax in fp32 (exp2 domain, lazy rescaling);
 //                     V rows are loaded coalesced (4 rows x 256 B per
 //                     instruction) and transposed in registers with byte
 //                     permutes into the A operand of
 //                     v_mfma_f32_16x16x16_bf16, whose B operand is P exactly
 //                     as the score MFMA left it (P split into bf16 hi + lo).
+//                   A wave's K/V stream runs on across pieces: the next
+//                   piece's descriptor comes from scalar loads, its page ids
+//                   and Q are loaded a piece ahead, and its first page while
+//                   the current piece's last page is consumed.  Piece results
+//                   wait in LDS (up to 64 / G per wave) and are written when
+//                   the wave's work is done, so no stores interleave with the
+//                   stream.
 //   combine_kernel  log-sum-exp merge of each listed segment's partials
 //                   (zeros for requests without tokens).
 //
@@ -64,7 +71,6 @@ constexpr int kMaxResidentGroups = 4096;
 constexpr int kPlanThreads = 1024;
 constexpr int kHeadsPerGroup = 4;      // preferred KV heads (waves) per attention workgroup
 constexpr int kAttnGroupsPerCU = 1;    // resident attention workgroups per CU
-constexpr int kPrefetch = 2;           // pages in flight per wave (ring of page tiles)
 constexpr int kAttnMaxThreads = 64 * kHeadsPerGroup;
 constexpr int kCombineThreads = 256;
 constexpr int kCombineGroupsPerCU = 4;
@@ -388,247 +394,413 @@ struct PageIds {
     }
 };
 
+// Clamped to the piece's last page, so every lane loads (no branches) and the
+// loads are counted the same way on every path.
 __device__ inline PageIds load_page_ids(const int32_t *pt_row, int jb, int je, int lane)
 {
     PageIds p;
 #pragma unroll
-    for (int x = 0; x < kMaxRangeTiles / 64; ++x) {
-        const int j = jb + 64 * x + lane;
-        p.win[x] = j < je ? pt_row[j] : 0;
-    }
+    for (int x = 0; x < kMaxRangeTiles / 64; ++x)
+        p.win[x] = pt_row[min(jb + 64 * x + lane, je - 1)];
     return p;
 }
 
-// One piece: pages [jb, je) of KV head g of request b (je - jb <= kMaxRangeTiles).
-template <int G, int MODE>
-__device__ inline void attn_piece(const AttnArgs &a, int b, int g, int jb, int je, int L,
-                                  bool whole, long long slot, int lane)
-{
-    const int r = lane & 15;    // score MFMA: token row (A) / head column (B, D)
-    const int grp = lane >> 4;  // lane group: k-slice of the operands, row block of D
-    const int Hkv = a.Hkv;
-    const unsigned row = (unsigned)Hkv * kHeadDim;        // elements per token row
-    const size_t page_elems = (size_t)kPage * row;
-    const PageIds ids = load_page_ids(a.pt + (size_t)b * a.pt_stride, jb, je, lane);
-    const unsigned koff = r * row + g * kHeadDim + 8 * grp;
-    const unsigned voff = 4 * grp * row + g * kHeadDim + 8 * r;
-    const uint16_t *kb = a.k, *vb = a.v;
-    const int np = je - jb;
+// Plan tables and request lengths are not written while the attention kernel
+// runs: read them through the constant address space, which gives scalar
+// loads that are counted apart from the K/V stream.
+typedef const __attribute__((address_space(4))) int32_t *const_i32p;
 
-    if constexpr (MODE == MODE_GATHER) {
-        uint16_t *ko = (uint16_t *)a.out;
-        uint16_t *vo = (uint16_t *)a.out2;
-        const long long t0 = a.tok_base[b];
-        for (int j = jb; j < je; ++j) {
-            const int pg = ids.get(j - jb);
-            Tile T;
-            load_tile(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems, koff, voff, row);
-            const int valid = L - j * kPage;
-            // K: the score operand as loaded, lane row r
-            if (r < valid) {
-                uint16_t *dst = ko + (size_t)(t0 + j * kPage + r) * row + g * kHeadDim + 8 * grp;
-#pragma unroll
-                for (int kk = 0; kk < 4; ++kk)
-                    *(u32x4 *)(dst + 32 * kk) = T.k[kk];
-            }
-            // V: rebuild each token row chunk from the transposed operands
-            s16x4 op[8];
-#pragma unroll
-            for (int blk = 0; blk < 8; ++blk)
-                op[blk] = v_operand(T, blk);
-#pragma unroll
-            for (int jj = 0; jj < 4; ++jj) {
-                if (4 * grp + jj < valid) {
-                    u32x4 w;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        w[e] = (unsigned)(unsigned short)op[2 * e][jj] |
-                               ((unsigned)(unsigned short)op[2 * e + 1][jj] << 16);
-                    *(u32x4 *)(vo + (size_t)(t0 + j * kPage + 4 * grp + jj) * row + g * kHeadDim +
-                               8 * r) = w;
-                }
-            }
-        }
-        return;
-    } else {
-        // Q operand (B of the score MFMA): head column r, d slice 8(4kk+grp)
-        u32x4 qreg[4];
-        const uint16_t *qrow = a.q + ((size_t)b * a.Hq + g * G + r) * kHeadDim + 8 * grp;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-            qreg[kk] = (r < G) ? ldg16(qrow + 32 * kk) : u32x4{0u, 0u, 0u, 0u};
+// A piece: pages [jb, je) of KV-head group q of request b, cut from range w.
+struct Piece {
+    int b, q, jb, je, L, w;
+};
 
-        f32x4 acc[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-        float m_run = -INFINITY;   // running max (log2 units) of head r
-        float l_run = 0.f;         // this lane's share of the normaliser
+// Walks the ranges of one workgroup (blockIdx.x, + gridDim.x, ...) and the
+// pieces each range covers, in order.
+struct PieceWalk {
+    int w, t_end, b, q, j, t;
 
-        auto page_step = [&](const Tile &T, int j) {
-            f32x4 s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk)
-                s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                    __builtin_bit_cast(bf16x8, T.k[kk]), __builtin_bit_cast(bf16x8, qreg[kk]),
-                    s, 0, 0, 0);
-            // s[i]: token 4grp+i, head r
-            float sc[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                sc[i] = s[i] * a.scale_log2;
-            Tile V = T;
-            const int valid = L - j * kPage;
-            if (valid < kPage) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    if (4 * grp + i >= valid) {
-                        sc[i] = -INFINITY;
-                        V.v[i] = u32x4{0u, 0u, 0u, 0u};
-                    }
-                }
+    __device__ inline bool next(const AttnArgs &a, int W, int Hg, Piece &p)
+    {
+        const const_i32p ranges = (const_i32p)a.ranges;   // {b, q, j, t} per range
+        const const_i32p lens = (const_i32p)a.seq_lens;
+        while (true) {
+            if (t >= t_end) {
+                w += gridDim.x;
+                if (w >= W)
+                    return false;
+                b = ranges[4 * w];
+                q = ranges[4 * w + 1];
+                j = ranges[4 * w + 2];
+                t = ranges[4 * w + 3];
+                t_end = ranges[4 * w + 7];
+                continue;
             }
-            float tmax = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-            tmax = wave_max_groups(tmax);
-            const bool need = tmax > m_run + kRescaleSlack;
-            if (__builtin_amdgcn_ballot_w64(need)) {
-                const float m_new = need ? tmax : m_run;
-                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-                l_run *= alpha;
-#pragma unroll
-                for (int i = 0; i < 8; ++i)
-                    acc[i] *= alpha;
-                m_run = m_new;
-            }
-            s16x4 phi, plo;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float p = __builtin_amdgcn_exp2f(sc[i] - m_run);
-                const unsigned short h = bf16_bits(p);
-                const float hf = bf16_val(h);
-                const unsigned short lo = bf16_bits(p - hf);
-                l_run += hf + bf16_val(lo);
-                phi[i] = (short)h;
-                plo[i] = (short)lo;
-            }
-#pragma unroll
-            for (int blk = 0; blk < 8; ++blk) {
-                const s16x4 vop = v_operand(V, blk);
-                acc[blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, phi, acc[blk], 0, 0, 0);
-                acc[blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, plo, acc[blk], 0, 0, 0);
-            }
-        };
-
-        // Page loop over a ring of kPrefetch tiles with a fixed trip count: the
-        // loads of page j + kPrefetch - 1 are issued before page j is consumed
-        // (the scheduling barriers keep the compiler from sinking them).
-        // Prefetches past the end re-read the final page, which the caches
-        // serve; every path issues the same loads, so the wait counts stay
-        // exact.
-        auto load_page = [&](Tile &T, int jn) {
-            const int pg = ids.get(min(jn, je - 1) - jb);
-            load_tile(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems, koff, voff, row);
-        };
-        Tile ring[kPrefetch];
-#pragma unroll
-        for (int u = 0; u < kPrefetch - 1; ++u)
-            load_page(ring[u], jb + u);
-        int j = jb;
-        for (int it = np / kPrefetch; it > 0; --it) {
-#pragma unroll
-            for (int u = 0; u < kPrefetch; ++u) {
-                load_page(ring[(u + kPrefetch - 1) % kPrefetch], j + u + kPrefetch - 1);
-                __builtin_amdgcn_sched_barrier(0);
-                page_step(ring[u], j + u);
-            }
-            j += kPrefetch;
-        }
-#pragma unroll
-        for (int u = 0; u < kPrefetch - 1; ++u)
-            if (u < np - (j - jb))
-                page_step(ring[u], j + u);
-
-        const float l_tot = sum_groups(l_run);
-        // acc[blk][i] = O[head r][d 32grp + 8i + blk]
-        if (r < G) {
-            const int h = g * G + r;
-            if (whole) {
-                const float inv = 1.0f / l_tot;
-                if constexpr (MODE == MODE_F32) {
-                    float *o = (float *)a.out + ((size_t)b * a.Hq + h) * kHeadDim + 32 * grp;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        f32x4 w0, w1;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            w0[e] = acc[e][i] * inv;
-                            w1[e] = acc[4 + e][i] * inv;
-                        }
-                        *(f32x4 *)(o + 8 * i) = w0;
-                        *(f32x4 *)(o + 8 * i + 4) = w1;
-                    }
-                } else {
-                    uint16_t *o = (uint16_t *)a.out + ((size_t)b * a.Hq + h) * kHeadDim + 32 * grp;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        u32x4 w;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            w[e] = (unsigned)bf16_bits(acc[2 * e][i] * inv) |
-                                   ((unsigned)bf16_bits(acc[2 * e + 1][i] * inv) << 16);
-                        *(u32x4 *)(o + 8 * i) = w;
-                    }
-                }
-            } else {
-                float *o = a.part_acc + ((size_t)slot * G + r) * kHeadDim + 32 * grp;
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    f32x4 w0, w1;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        w0[e] = acc[e][i];
-                        w1[e] = acc[4 + e][i];
-                    }
-                    *(f32x4 *)(o + 8 * i) = w0;
-                    *(f32x4 *)(o + 8 * i + 4) = w1;
-                }
-                if (grp == 0)
-                    a.part_ml[(size_t)slot * G + r] = make_float2(m_run, l_tot);
-            }
-        }
-    }
-}
-
-template <int G, int MODE>
-__global__ void __launch_bounds__(kAttnMaxThreads)
-attn_kernel(const AttnArgs a)
-{
-    const int lane = threadIdx.x & 63;
-    const int hi = threadIdx.x >> 6;          // head within the group
-    const int W = a.hdr->n_ranges;
-    const int HW = a.HW, Hg = a.Hkv / a.HW;
-    for (int w = blockIdx.x; w < W; w += gridDim.x) {
-        const int4 rs = a.ranges[w];
-        const int t_end = a.ranges[w + 1].w;
-        int b = rs.x, q = rs.y, j = rs.z, t = rs.w;
-        while (t < t_end) {
-            const int L = min(a.seq_lens[b], a.maxp * kPage);
+            const int L = min(lens[b], a.maxp * kPage);
             const int P = L > 0 ? (L + kPage - 1) / kPage : 0;
             if (P == 0) {   // request without tokens: no tiles
                 ++b;
                 continue;
             }
             const int n = min(P - j, t_end - t);
-            const long long segment = (long long)b * Hg + q;
-            attn_piece<G, MODE>(a, b, q * HW + hi, j, j + n, L, j == 0 && n == P,
-                                (w + segment) * HW + hi, lane);
+            p = Piece{b, q, j, j + n, L, w};
             t += n;
             j = 0;
             if (++q == Hg) {
                 q = 0;
                 ++b;
             }
+            return true;
         }
+    }
+};
+
+// Q operand (B of the score MFMA): head column r, d slice 8(4kk+grp).  Columns
+// r >= G repeat head G-1; their results are never stored.
+template <int G>
+__device__ inline void load_q(const AttnArgs &a, int b, int g, int lane, u32x4 (&qreg)[4])
+{
+    const int r = min(lane & 15, G - 1), grp = lane >> 4;
+    const uint16_t *qrow = a.q + ((size_t)b * a.Hq + g * G + r) * kHeadDim + 8 * grp;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+        qreg[kk] = ldg16(qrow + 32 * kk);
+}
+
+// Copy-through gather of one piece (je - jb <= kMaxRangeTiles) for KV head
+// g = q * HW + hi; its page ids were loaded during the previous piece.
+__device__ inline void gather_piece(const AttnArgs &a, const Piece &pc, const PageIds &ids, int hi,
+                                    int lane)
+{
+    const int r = lane & 15;    // score MFMA: token row (A) / head column (B, D)
+    const int grp = lane >> 4;  // lane group: k-slice of the operands, row block of D
+    const int Hkv = a.Hkv;
+    const int b = pc.b, g = pc.q * a.HW + hi, jb = pc.jb, je = pc.je, L = pc.L;
+    const unsigned row = (unsigned)Hkv * kHeadDim;        // elements per token row
+    const size_t page_elems = (size_t)kPage * row;
+    const unsigned koff = r * row + g * kHeadDim + 8 * grp;
+    const unsigned voff = 4 * grp * row + g * kHeadDim + 8 * r;
+    const uint16_t *kb = a.k, *vb = a.v;
+
+    uint16_t *ko = (uint16_t *)a.out;
+    uint16_t *vo = (uint16_t *)a.out2;
+    const long long t0 = a.tok_base[b];
+    for (int j = jb; j < je; ++j) {
+        const int pg = ids.get(j - jb);
+        Tile T;
+        load_tile(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems, koff, voff, row);
+        const int valid = L - j * kPage;
+        // K: the score operand as loaded, lane row r
+        if (r < valid) {
+            uint16_t *dst = ko + (size_t)(t0 + j * kPage + r) * row + g * kHeadDim + 8 * grp;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk)
+                *(u32x4 *)(dst + 32 * kk) = T.k[kk];
+        }
+        // V: rebuild each token row chunk from the transposed operands
+        s16x4 op[8];
+#pragma unroll
+        for (int blk = 0; blk < 8; ++blk)
+            op[blk] = v_operand(T, blk);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+            if (4 * grp + jj < valid) {
+                u32x4 w;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    w[e] = (unsigned)(unsigned short)op[2 * e][jj] |
+                           ((unsigned)(unsigned short)op[2 * e + 1][jj] << 16);
+                *(u32x4 *)(vo + (size_t)(t0 + j * kPage + 4 * grp + jj) * row + g * kHeadDim +
+                           8 * r) = w;
+            }
+        }
+    }
+}
+
+// Attention over one piece (je - jb <= kMaxRangeTiles) for KV head
+// g = q * HW + hi.  Page tiles go through a two-slot ring: the load of page
+// s + 1 is issued before page s is consumed, and the last page's step issues
+// the load of the next piece's first page.  The piece's first page is in slot
+// PH (loaded by the previous piece); the next piece's lands in slot
+// PH ^ (np & 1), which the function returns as np & 1.  The first and last
+// steps are written out apart from the loop, so every load is waited for with
+// an exact count.  fetch_next() walks to the next piece and loads its page
+// ids and Q operand (into nids / the caller's registers) before the first
+// step.
+template <int G, int MODE, int PH, typename Fetch>
+__device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageIds &ids,
+                                 const u32x4 (&qreg)[4], Tile (&ring)[2], Fetch &&fetch_next,
+                                 const PageIds &nids, const Piece &nxt, int hi, int lane,
+                                 float *entry, float2 *entry_ml)
+{
+    const int r = lane & 15;    // score MFMA: token row (A) / head column (B, D)
+    const int grp = lane >> 4;  // lane group: k-slice of the operands, row block of D
+    const int Hkv = a.Hkv;
+    const int g = pc.q * a.HW + hi, jb = pc.jb, je = pc.je, L = pc.L;
+    const unsigned row = (unsigned)Hkv * kHeadDim;        // elements per token row
+    const size_t page_elems = (size_t)kPage * row;
+    const unsigned koff = r * row + g * kHeadDim + 8 * grp;
+    const unsigned voff = 4 * grp * row + g * kHeadDim + 8 * r;
+    const uint16_t *kb = a.k, *vb = a.v;
+    const int np = je - jb;
+
+    fetch_next();
+
+    f32x4 acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY;   // running max (log2 units) of head r
+    float l_run = 0.f;         // this lane's share of the normaliser
+
+    auto page_step = [&](const Tile &T, int j) {
+        f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, T.k[kk]), __builtin_bit_cast(bf16x8, qreg[kk]),
+                s, 0, 0, 0);
+        // s[i]: token 4grp+i, head r
+        float sc[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            sc[i] = s[i] * a.scale_log2;
+        Tile V = T;
+        const int valid = L - j * kPage;
+        if (valid < kPage) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (4 * grp + i >= valid) {
+                    sc[i] = -INFINITY;
+                    V.v[i] = u32x4{0u, 0u, 0u, 0u};
+                }
+            }
+        }
+        float tmax = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
+        tmax = wave_max_groups(tmax);
+        const bool need = tmax > m_run + kRescaleSlack;
+        if (__builtin_amdgcn_ballot_w64(need)) {
+            const float m_new = need ? tmax : m_run;
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            l_run *= alpha;
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                acc[i] *= alpha;
+            m_run = m_new;
+        }
+        s16x4 phi, plo;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float p = __builtin_amdgcn_exp2f(sc[i] - m_run);
+            const unsigned short h = bf16_bits(p);
+            const float hf = bf16_val(h);
+            const unsigned short lo = bf16_bits(p - hf);
+            l_run += hf + bf16_val(lo);
+            phi[i] = (short)h;
+            plo[i] = (short)lo;
+        }
+#pragma unroll
+        for (int blk = 0; blk < 8; ++blk) {
+            const s16x4 vop = v_operand(V, blk);
+            acc[blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, phi, acc[blk], 0, 0, 0);
+            acc[blk] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vop, plo, acc[blk], 0, 0, 0);
+        }
+    };
+
+    auto load_in = [&](Tile &T, int jn) {   // page jn of this piece
+        const int pg = ids.get(jn - jb);
+        load_tile(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems, koff, voff, row);
+    };
+    auto load_next = [&](Tile &T) {         // first page of the next piece
+        const int ng = nxt.q * a.HW + hi;
+        const int pg = nids.get(0);
+        load_tile(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems,
+                  r * row + ng * kHeadDim + 8 * grp, 4 * grp * row + ng * kHeadDim + 8 * r, row);
+    };
+    constexpr int A = PH, B = PH ^ 1;
+    if (np >= 2) {
+        load_in(ring[B], jb + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        page_step(ring[A], jb);
+        int s = jb + 1;
+        for (int it = (np - 2) / 2; it > 0; --it) {
+            load_in(ring[A], s + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            page_step(ring[B], s);
+            load_in(ring[B], s + 2);
+            __builtin_amdgcn_sched_barrier(0);
+            page_step(ring[A], s + 1);
+            s += 2;
+        }
+    }
+    if (np & 1) {
+        if (np >= 3) {
+            load_in(ring[A], je - 1);
+            __builtin_amdgcn_sched_barrier(0);
+            page_step(ring[B], je - 2);
+        }
+        load_next(ring[B]);
+        __builtin_amdgcn_sched_barrier(0);
+        page_step(ring[A], je - 1);
+    } else {
+        load_next(ring[A]);
+        __builtin_amdgcn_sched_barrier(0);
+        page_step(ring[B], je - 1);
+    }
+
+    const float l_tot = sum_groups(l_run);
+    // acc[blk][i] = O[head r][d 32grp + 8i + blk].  The results go to this
+    // wave's LDS entry (lanes r < G hold head r): normalised for a whole
+    // segment, else raw with (max, normaliser).  They reach global memory
+    // in a batch later, so the K/V stream carries no stores.
+    const bool whole = jb == 0 && je == (L + kPage - 1) / kPage;
+    const float sc = whole ? 1.0f / l_tot : 1.0f;
+    if (r < G) {
+        float *srow = entry + r * kHeadDim + 32 * grp;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            f32x4 w0, w1;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                w0[e] = acc[e][i] * sc;
+                w1[e] = acc[4 + e][i] * sc;
+            }
+            *(f32x4 *)(srow + 8 * i) = w0;
+            *(f32x4 *)(srow + 8 * i + 4) = w1;
+        }
+        entry_ml[r] = make_float2(m_run, l_tot);
+    }
+    return np & 1;
+}
+
+// Each workgroup walks its ranges piece by piece, HW waves per piece (one KV
+// head each).  The next piece's descriptor (scalar loads), page ids and Q
+// operand are loaded at the start of a piece, and its first page while the
+// piece's last page is consumed, so the K/V stream of a wave runs on across
+// piece boundaries.
+template <int G, int MODE>
+__global__ void __launch_bounds__(kAttnMaxThreads)
+attn_kernel(const AttnArgs a)
+{
+    const int lane = threadIdx.x & 63;
+    const int hi = threadIdx.x >> 6;          // KV head within the group
+    const int W = a.hdr->n_ranges;
+    const int HW = a.HW, Hg = a.Hkv / a.HW;
+    PieceWalk walk{(int)blockIdx.x - (int)gridDim.x, 0, 0, 0, 0, 0};
+    Piece cur;
+    if (!walk.next(a, W, Hg, cur))
+        return;
+    PageIds ids = load_page_ids(a.pt + (size_t)cur.b * a.pt_stride, cur.jb, cur.je, lane);
+    if constexpr (MODE == MODE_GATHER) {
+        while (true) {
+            Piece nxt;
+            const bool more = walk.next(a, W, Hg, nxt);
+            if (!more)
+                nxt = cur;
+            const PageIds nids =
+                load_page_ids(a.pt + (size_t)nxt.b * a.pt_stride, nxt.jb, nxt.je, lane);
+            gather_piece(a, cur, ids, hi, lane);
+            if (!more)
+                break;
+            cur = nxt;
+            ids = nids;
+        }
+    } else {
+        // Per wave: up to kDefer piece results, written out when the wave's
+        // work is done (or when all entries are taken).
+        constexpr int kDefer = 64 / G;
+        __shared__ float s_res[kHeadsPerGroup][kDefer][G * kHeadDim];
+        __shared__ float2 s_ml[kHeadsPerGroup][kDefer][G];
+        __shared__ int2 s_meta[kHeadsPerGroup][kDefer];   // {whole, out row or partial slot}
+        int n_res = 0;
+        auto flush = [&]() {
+            constexpr int kF32Chunks = G * kHeadDim / 4, kBf16Chunks = G * kHeadDim / 8;
+            for (int e = 0; e < n_res; ++e) {
+                const int2 m = s_meta[hi][e];
+                const int whole = __builtin_amdgcn_readfirstlane(m.x);
+                const int tgt = __builtin_amdgcn_readfirstlane(m.y);
+                const float *st = s_res[hi][e];
+                if (whole && MODE == MODE_BF16) {
+                    uint16_t *o = (uint16_t *)a.out + (size_t)tgt * kHeadDim;
+#pragma unroll
+                    for (int c0 = 0; c0 < kBf16Chunks; c0 += 64) {
+                        const int c = c0 + (kBf16Chunks >= 64 ? lane : (lane & (kBf16Chunks - 1)));
+                        const f32x4 x0 = *(const f32x4 *)(st + 8 * c);
+                        const f32x4 x1 = *(const f32x4 *)(st + 8 * c + 4);
+                        u32x4 w;
+                        w[0] = (unsigned)bf16_bits(x0[0]) | ((unsigned)bf16_bits(x0[1]) << 16);
+                        w[1] = (unsigned)bf16_bits(x0[2]) | ((unsigned)bf16_bits(x0[3]) << 16);
+                        w[2] = (unsigned)bf16_bits(x1[0]) | ((unsigned)bf16_bits(x1[1]) << 16);
+                        w[3] = (unsigned)bf16_bits(x1[2]) | ((unsigned)bf16_bits(x1[3]) << 16);
+                        *(u32x4 *)(o + 8 * c) = w;
+                    }
+                } else {
+                    float *o = whole ? (float *)a.out + (size_t)tgt * kHeadDim
+                                     : a.part_acc + (size_t)tgt * G * kHeadDim;
+#pragma unroll
+                    for (int c0 = 0; c0 < kF32Chunks; c0 += 64) {
+                        const int c = c0 + (kF32Chunks >= 64 ? lane : (lane & (kF32Chunks - 1)));
+                        *(f32x4 *)(o + 4 * c) = *(const f32x4 *)(st + 4 * c);
+                    }
+                    if (!whole) {
+                        const int hh = lane & (G - 1);
+                        a.part_ml[(size_t)tgt * G + hh] = s_ml[hi][e][hh];
+                    }
+                }
+            }
+            n_res = 0;
+        };
+        u32x4 qreg[4];
+        load_q<G>(a, cur.b, cur.q * HW + hi, lane, qreg);
+        Tile ring[2];
+        {   // first page of the first piece
+            const unsigned row = (unsigned)a.Hkv * kHeadDim;
+            const int r = lane & 15, grp = lane >> 4, g = cur.q * HW + hi;
+            const size_t pg = (size_t)ids.get(0) * kPage * row;
+            load_tile(ring[0], a.k + pg, a.v + pg, r * row + g * kHeadDim + 8 * grp,
+                      4 * grp * row + g * kHeadDim + 8 * r, row);
+        }
+        int ph = 0;
+        while (true) {
+            Piece nxt;
+            bool more = false;
+            PageIds nids;
+            u32x4 nq[4];
+            auto fetch_next = [&]() {
+                more = walk.next(a, W, Hg, nxt);
+                if (!more) {   // last piece: the final prefetch re-reads its last page
+                    nxt = cur;
+                    nxt.jb = cur.je - 1;
+                }
+                nids = load_page_ids(a.pt + (size_t)nxt.b * a.pt_stride, nxt.jb, nxt.je, lane);
+                load_q<G>(a, nxt.b, nxt.q * HW + hi, lane, nq);
+            };
+            if (n_res == kDefer)
+                flush();
+            float *entry = s_res[hi][n_res];
+            float2 *entry_ml = s_ml[hi][n_res];
+            const int flip =
+                ph == 0 ? attn_piece<G, MODE, 0>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml)
+                        : attn_piece<G, MODE, 1>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml);
+            {
+                const int g = cur.q * HW + hi;
+                const bool whole = cur.jb == 0 && cur.je == (cur.L + kPage - 1) / kPage;
+                const long long slot = ((long long)cur.w + (long long)cur.b * Hg + cur.q) * HW + hi;
+                s_meta[hi][n_res] = make_int2(whole ? 1 : 0,
+                                              whole ? cur.b * a.Hq + g * G : (int)slot);
+                ++n_res;
+            }
+            if (!more)
+                break;
+            ph ^= flip;
+            cur = nxt;
+            ids = nids;
+            qreg[0] = nq[0];
+            qreg[1] = nq[1];
+            qreg[2] = nq[2];
+            qreg[3] = nq[3];
+        }
+        flush();
     }
 }
 

@@ -269,6 +269,21 @@ def test_max_requests():
     check_f32(run_gpu(d), ref, "8192 requests")
 
 
+@pytest.mark.parametrize("G,hkv", [(16, 1), (16, 2), (8, 2)])
+def test_many_pieces_per_wave(G, hkv):
+    """Thousands of short requests: a wave finishes more pieces than it can
+    hold results for in LDS (64 / G), so results are written out mid-stream
+    as well as at the end."""
+    rng = np.random.default_rng(50 + G + hkv)
+    lengths = [int(x) for x in rng.choice([1, 3, 16, 17, 40, 100], 3000)]
+    say("case: 3000 short requests, G=%d Hkv=%d, N_kv %d" % (G, hkv, sum(lengths)))
+    c = custom(lengths, hq=G * hkv, hkv=hkv, seed=51 + G)
+    d = dev_case(c)
+    ref = ref_of(c)
+    check_f32(run_gpu(d), ref, "many pieces G=%d" % G)
+    check_bf16(run_gpu(d, torch.bfloat16), ref, "many pieces G=%d" % G)
+
+
 def test_sixteen_kv_heads():
     say("case: 32:16 heads and 16:16 heads")
     for hq, hkv in ((32, 16), (16, 16)):
