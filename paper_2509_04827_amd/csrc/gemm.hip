@@ -26,6 +26,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <stdint.h>
 
 #include "vdecode.h"
@@ -199,6 +200,31 @@ gemm_reduce_kernel(const float *__restrict__ part, void *__restrict__ y, size_t 
 
 bool aligned(const void *p, size_t al) { return ((uintptr_t)p & (al - 1)) == 0; }
 
+// Compute units of the current device, queried once per device (0 = not yet).
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];
+
+int device_cus(int *cus)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return VD_ERROR_LAUNCH;
+    if (dev >= 0 && dev < kMaxDevices) {
+        const int v = g_cus[dev].load(std::memory_order_relaxed);
+        if (v > 0) {
+            *cus = v;
+            return VD_SUCCESS;
+        }
+    }
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        return VD_ERROR_LAUNCH;
+    if (dev >= 0 && dev < kMaxDevices)
+        g_cus[dev].store(n, std::memory_order_relaxed);
+    *cus = n;
+    return VD_SUCCESS;
+}
+
 int gemm_check(int M, int N, int K, unsigned flags)
 {
     if (M <= 0 || N <= 0 || K <= 0)
@@ -259,9 +285,8 @@ int vd_gemm_bf16(const void *x, const void *w, void *y, int M, int N, int K, voi
         return st;
     if (!x || !w || !y || !aligned(x, 16) || !aligned(w, 16) || !aligned(y, 16))
         return VD_ERROR_INVALID_VALUE;
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    int cus = 0;
+    if (device_cus(&cus) != VD_SUCCESS)
         return VD_ERROR_LAUNCH;
     const int S = gemm_slices(M, N, K, cus);
     if (S > 1) {

@@ -55,6 +55,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <stdint.h>
 
@@ -1029,14 +1030,27 @@ int launch_status()
     return hipGetLastError() == hipSuccess ? VD_SUCCESS : VD_ERROR_LAUNCH;
 }
 
+// Compute units of the current device, queried once per device (0 = not yet).
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_cus[kMaxDevices];
+
 int num_cus(int *out)
 {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess)
         return VD_ERROR_LAUNCH;
+    if (dev >= 0 && dev < kMaxDevices) {
+        const int v = g_cus[dev].load(std::memory_order_relaxed);
+        if (v > 0) {
+            *out = v;
+            return VD_SUCCESS;
+        }
+    }
     int n = 0;
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
         return VD_ERROR_LAUNCH;
+    if (dev >= 0 && dev < kMaxDevices)
+        g_cus[dev].store(n, std::memory_order_relaxed);
     *out = n;
     return VD_SUCCESS;
 }
@@ -1058,10 +1072,37 @@ const void *attn_kernel_ptr(int G, int mode)
 #undef VD_K
 }
 
+int log2_pow2(int x)
+{
+    int l = 0;
+    while ((1 << l) < x)
+        ++l;
+    return l;
+}
+
+// Resident attention workgroups per (device, G, mode, HW), queried once: the
+// occupancy query costs more host time than a small step's kernels.  0 means
+// not queried yet; concurrent first calls store the same value.
+std::atomic<int> g_resident[kMaxDevices][5][3][3];
+
 // Workgroups of the attention kernel (HW waves each) that fit on the device
 // at once.
 int resident_attn_groups(int G, int mode, int HW, int *groups)
 {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return VD_ERROR_LAUNCH;
+    const int gi = log2_pow2(G), hwi = log2_pow2(HW);
+    std::atomic<int> *slot = (dev >= 0 && dev < kMaxDevices && gi < 5 && mode < 3 && hwi < 3)
+                                 ? &g_resident[dev][gi][mode][hwi]
+                                 : nullptr;
+    if (slot) {
+        const int v = slot->load(std::memory_order_relaxed);
+        if (v > 0) {
+            *groups = v;
+            return VD_SUCCESS;
+        }
+    }
     int cus = 0;
     int st = num_cus(&cus);
     if (st)
@@ -1074,6 +1115,8 @@ int resident_attn_groups(int G, int mode, int HW, int *groups)
         per_cu <= 0)
         return VD_ERROR_LAUNCH;
     *groups = std::min(cus * std::min(per_cu, kAttnGroupsPerCU), kMaxResidentGroups);
+    if (slot)
+        slot->store(*groups, std::memory_order_relaxed);
     return VD_SUCCESS;
 }
 
@@ -1256,7 +1299,9 @@ int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, in
     st = num_cus(&cus);
     if (st)
         return st;
-    const dim3 grid((unsigned)(cus * kCombineGroupsPerCU));
+    // work items: at most one per (request, query head)
+    const long long items = std::max(1LL, (long long)num_seqs * n_q_heads);
+    const dim3 grid((unsigned)std::min<long long>((long long)cus * kCombineGroupsPerCU, items));
     if (flags & VD_FLAG_OUT_F32)
         hipLaunchKernelGGL(combine_kernel<MODE_F32>, grid, dim3(kCombineThreads), 0, stream, c);
     else
