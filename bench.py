@@ -413,8 +413,14 @@ def main():
             if time.time() >= t_end or len(times) >= 5:
                 break
         sec = float(np.median(times))
+        cpu_model = None
+        try:
+            with open("/proc/cpuinfo") as f:
+                cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+        except OSError:
+            pass
         cpu = {"value": round(kvb / sec / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
-               "kind": "oracle",
+               "kind": "oracle", "cpu_model": cpu_model, "nproc": os.cpu_count(),
                "sample": "the whole %s step (all %d requests, %d KV tokens), fp64, %d run(s), "
                          "median %.2f s" % (w.name, B, c["n_kv"], len(times), sec)}
 

@@ -1017,10 +1017,12 @@ int check_shapes(int num_seqs, int n_q_heads, int n_kv_heads, int head_dim, int 
     if (head_dim != kHeadDim || page_size != kPage || !supported_g(n_q_heads / n_kv_heads) ||
         num_seqs > kMaxSeqs)
         return VD_ERROR_NOT_SUPPORTED;
-    // 32-bit in-page offsets, tile counts and token counts
+    // 32-bit in-page offsets, tile counts, token counts, output rows and
+    // partial slots (fewer than (maxp + 1) * B * Hkv)
     if ((long long)n_kv_heads * kHeadDim * kPage >= (1LL << 30) ||
-        (long long)num_seqs * max_pages_per_seq * n_kv_heads >= (1LL << 31) ||
-        (long long)num_seqs * max_pages_per_seq >= (1LL << 31) / kPage)
+        (long long)num_seqs * (max_pages_per_seq + 1) * n_kv_heads >= (1LL << 31) ||
+        (long long)num_seqs * max_pages_per_seq >= (1LL << 31) / kPage ||
+        (long long)num_seqs * n_q_heads >= (1LL << 31))
         return VD_ERROR_NOT_SUPPORTED;
     return VD_SUCCESS;
 }

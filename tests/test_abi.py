@@ -87,6 +87,9 @@ def test_argument_errors(entry):
     assert call_attn(fn, Hq=24, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     assert call_attn(fn, Hq=256, Hkv=8, **ok) == vd.VD_ERROR_NOT_SUPPORTED   # G = 32
     assert call_attn(fn, B=9000, **ok) == vd.VD_ERROR_NOT_SUPPORTED
+    # output rows (request, query head) and partial slots must fit 32 bits
+    assert call_attn(fn, B=8192, Hq=262144, Hkv=16384, maxp=1, **ok) == vd.VD_ERROR_NOT_SUPPORTED
+    assert call_attn(fn, B=8192, Hq=16384, Hkv=8192, maxp=31, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     assert call_attn(fn, wsb=need - 1) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
     assert call_attn(fn, wsb=0) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
     forced = vd.VD_FLAG_RANGE_TILES(1)
