@@ -12,10 +12,12 @@
 //     for batches up to 8 rows, 4 above, where the x rows are re-read less
 //     often) and a slice of K; its four waves take a quarter of the slice
 //     each and merge their accumulators in LDS in a fixed order;
-//   * a wave loads 16-byte fragments of the weight rows straight into the B
-//     operand of v_mfma_f32_16x16x32_bf16 (lane = output column) and of the
-//     x rows into the A operand (lane = batch row), four K steps per batch,
-//     two batches in flight;
+//   * a wave loads the weight rows in whole 128-byte pieces (8 rows per
+//     instruction, 8 lanes per row) and moves them through its own LDS tile
+//     into the B operand of v_mfma_f32_16x16x32_bf16 (lane = output column):
+//     the operand layout itself would read 64 bytes per row per instruction,
+//     which streams 20-35% slower.  x rows go straight into the A operand
+//     (lane = batch row).  Four K steps per batch, two batches in flight;
 //   * when there are too few column tiles to fill the device, K is split
 //     over workgroups as well; each slice writes an fp32 partial and a second
 //     kernel adds the slices in order (deterministic, no atomics).
@@ -40,7 +42,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kGemmThreads = 256;             // four waves split the K slice
 constexpr int kTileN = 64;                    // column granularity of N (the widest tile)
 constexpr int kKStep = 32;                    // K per MFMA
-constexpr int kUnroll = 4;                    // K steps per load batch
+constexpr int kUnroll = 4;                    // K steps per load batch (the LDS tile assumes 4)
 constexpr int kBatchK = kKStep * kUnroll;     // 128
 constexpr int kSliceAlign = 4 * kBatchK;      // K slice granularity: 512
 constexpr int kMaxM = 64;
@@ -71,6 +73,10 @@ gemm_kernel(const GemmArgs a)
 {
     constexpr int kNB = NB;
     __shared__ f32x4 red[3][kNB * MB][64];
+    // per wave: the batch's weight rows, 16 rows x 256 B (+16 B against bank
+    // conflicts on the column reads) per block
+    static_assert(kUnroll == 4, "two row halves x two K halves per block");
+    __shared__ u32x4 wst[4][kNB][16][4 * kUnroll + 1];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, grp = lane >> 4;
     const int n0 = blockIdx.x * 16 * kNB;
@@ -79,10 +85,14 @@ gemm_kernel(const GemmArgs a)
     const int kb = slice * a.kslice + wave * kw;
     const int K = a.K, M = a.M;
 
-    const uint16_t *wp[kNB];
+    // loads: instruction (h, c) of a block reads rows 8h .. 8h+7, 128 B each
+    // (k 64c .. 64c+63 of the batch), lane l: row 8h + l/8, k 64c + 8 (l % 8)
+    const uint16_t *wp[kNB][2];
 #pragma unroll
     for (int nb = 0; nb < kNB; ++nb)
-        wp[nb] = a.w + (size_t)(n0 + 16 * nb + r) * K + kb + 8 * grp;
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            wp[nb][h] = a.w + (size_t)(n0 + 16 * nb + 8 * h + (lane >> 3)) * K + kb + 8 * (lane & 7);
     const uint16_t *xp[MB];
     bool xv[MB];
 #pragma unroll
@@ -96,7 +106,8 @@ gemm_kernel(const GemmArgs a)
         for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
             for (int nb = 0; nb < kNB; ++nb)
-                B.w[nb][u] = __builtin_nontemporal_load((const u32x4 *)(wp[nb] + koff + kKStep * u));
+                B.w[nb][u] = __builtin_nontemporal_load(
+                    (const u32x4 *)(wp[nb][u & 1] + koff + 64 * (u >> 1)));
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
@@ -113,15 +124,24 @@ gemm_kernel(const GemmArgs a)
             acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     auto compute = [&](const Batch<kNB, MB> &B) {
+        // through LDS into the B-operand layout: lane (r, grp) of K step u
+        // takes row r, 16-byte chunk 4u + grp
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb)
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+                wst[wave][nb][8 * (u & 1) + (lane >> 3)][8 * (u >> 1) + (lane & 7)] = B.w[nb][u];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
 #pragma unroll
-            for (int nb = 0; nb < kNB; ++nb)
+            for (int nb = 0; nb < kNB; ++nb) {
+                const u32x4 wf = wst[wave][nb][r][4 * u + grp];
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb)
                     acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8, B.x[mb][u]), __builtin_bit_cast(bf16x8, B.w[nb][u]),
+                        __builtin_bit_cast(bf16x8, B.x[mb][u]), __builtin_bit_cast(bf16x8, wf),
                         acc[nb][mb], 0, 0, 0);
+            }
     };
 
     // two batches in flight; past the end the prefetch re-reads the wave's
