@@ -339,19 +339,43 @@ __device__ inline void load_tile(Tile &T, const uint16_t *kpage, const uint16_t 
         T.v[j] = ldg16_stream(vp[j]);
 }
 
+// The lane-group exchanges use the gfx950 row swaps (VALU, no LDS): with
+// both operands x, v_permlane16_swap leaves rows {0,0,2,2} and {1,1,3,3} of
+// x in its two results, and v_permlane32_swap halves {lo,lo} and {hi,hi}.
+__device__ inline void swap16(float x, float &a, float &b)
+{
+    const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(unsigned, x),
+                                                    __builtin_bit_cast(unsigned, x), false, false);
+    a = __builtin_bit_cast(float, (unsigned)r[0]);
+    b = __builtin_bit_cast(float, (unsigned)r[1]);
+}
+
+__device__ inline void swap32(float x, float &a, float &b)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x),
+                                                    __builtin_bit_cast(unsigned, x), false, false);
+    a = __builtin_bit_cast(float, (unsigned)r[0]);
+    b = __builtin_bit_cast(float, (unsigned)r[1]);
+}
+
 __device__ inline float wave_max_groups(float x)
 {
     // max over the 4 lane groups that share lane & 15
-    x = fmaxf(x, __shfl_xor(x, 16));
-    x = fmaxf(x, __shfl_xor(x, 32));
-    return x;
+    float a, b;
+    swap16(x, a, b);
+    x = fmaxf(a, b);
+    swap32(x, a, b);
+    return fmaxf(a, b);
 }
 
 __device__ inline float sum_groups(float x)
 {
-    x += __shfl_xor(x, 16);
-    x += __shfl_xor(x, 32);
-    return x;
+    // (g0 + g1) + (g2 + g3) in every lane of the four groups
+    float a, b;
+    swap16(x, a, b);
+    x = a + b;
+    swap32(x, a, b);
+    return a + b;
 }
 
 __device__ inline unsigned short bf16_bits(float f)
@@ -528,7 +552,7 @@ __device__ inline void gather_piece(const AttnArgs &a, const Piece &pc, const Pa
 // an exact count.  fetch_next() walks to the next piece and loads its page
 // ids and Q operand (into nids / the caller's registers) before the first
 // step.
-template <int G, int MODE, int PH, typename Fetch>
+template <int G, int PH, typename Fetch>
 __device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageIds &ids,
                                  const u32x4 (&qreg)[4], Tile (&ring)[2], Fetch &&fetch_next,
                                  const PageIds &nids, const Piece &nxt, int hi, int lane,
@@ -781,8 +805,8 @@ attn_kernel(const AttnArgs a)
             float *entry = s_res[hi][n_res];
             float2 *entry_ml = s_ml[hi][n_res];
             const int flip =
-                ph == 0 ? attn_piece<G, MODE, 0>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml)
-                        : attn_piece<G, MODE, 1>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml);
+                ph == 0 ? attn_piece<G, 0>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml)
+                        : attn_piece<G, 1>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml);
             {
                 const int g = cur.q * HW + hi;
                 const bool whole = cur.jb == 0 && cur.je == (cur.L + kPage - 1) / kPage;
