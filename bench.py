@@ -130,13 +130,35 @@ def latency_surface(outdir: str, iters: int = 10, warmup: int = 3):
             step(e0, e1)
         torch.cuda.synchronize()
         us_attn = float(np.median([a.elapsed_time(b) for a, b in ev])) * 1e3
+        # the same step captured into a HIP graph and replayed: no host launch
+        # cost per kernel, so small steps show the device-side floor
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            vd.vd_decode_attn(q, kp, vp, ptd, sl, out, scale, ws)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            vd.vd_decode_attn(q, kp, vp, ptd, sl, out, scale, ws)
+        for _ in range(warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        st.record(stream)
+        for _ in range(iters):
+            graph.replay()
+        en.record(stream)
+        torch.cuda.synchronize()
+        us_graph = st.elapsed_time(en) * 1e3 / iters
+        del graph
         n_kv = int(lens.sum())
         kvb = n_kv * Hkv * D * 2 * 2
         rows.append(dict(law=law, n_q_heads=Hq, n_req=B, tokens_per_req=int(round(lens.mean())),
                          n_kv=n_kv, us_step=round(us_step, 2), us_attn=round(us_attn, 2),
+                         us_step_graph=round(us_graph, 2),
                          kv_gbs_step=round(kvb / us_step / 1e3, 1)))
-        print("surface %-8s Hq %2d B %4d L %6d N_kv %8d  step %9.2f us  attn %9.2f us  %7.1f GB/s"
-              % (law, Hq, B, lens.mean(), n_kv, us_step, us_attn, kvb / us_step / 1e3),
+        print("surface %-8s Hq %2d B %4d L %6d N_kv %8d  step %9.2f us  graph %9.2f us  attn %9.2f us  %7.1f GB/s"
+              % (law, Hq, B, lens.mean(), n_kv, us_step, us_graph, us_attn, kvb / us_step / 1e3),
               file=sys.stderr, flush=True)
 
     for B in SURFACE_BATCH:
@@ -155,20 +177,26 @@ def latency_surface(outdir: str, iters: int = 10, warmup: int = 3):
         f.write(",".join(keys) + "\n")
         for r in rows:
             f.write(",".join(str(r[k]) for k in keys) + "\n")
-    # Eq. pred-itl: T = c*N_req + d*N_kv + e, fitted on the 32:8 points
+    # Eq. pred-itl: T = c*N_req + d*N_kv + e, fitted on the 32:8 points, for
+    # eager steps and for graph replays
     sel = [r for r in rows if r["n_q_heads"] == 32]
     A = np.array([[r["n_req"], r["n_kv"], 1.0] for r in sel], dtype=np.float64)
-    y = np.array([r["us_step"] for r in sel])
-    coef, *_ = np.linalg.lstsq(A, y, rcond=None)
-    pred = A @ coef
-    r2 = 1.0 - ((y - pred) ** 2).sum() / ((y - y.mean()) ** 2).sum()
-    mae = float(np.abs(y - pred).mean())
-    bw = Hkv * D * 2 * 2 / (coef[1] * 1e-6) / 1e9
-    fit = dict(c_us_per_req=coef[0], d_us_per_kv_token=coef[1], e_us=coef[2], r2=r2, mae_us=mae,
-               implied_kv_gbs=bw, points=len(sel))
+
+    def fit_of(key):
+        y = np.array([r[key] for r in sel])
+        coef, *_ = np.linalg.lstsq(A, y, rcond=None)
+        pred = A @ coef
+        r2 = 1.0 - ((y - pred) ** 2).sum() / ((y - y.mean()) ** 2).sum()
+        mae = float(np.abs(y - pred).mean())
+        bw = Hkv * D * 2 * 2 / (coef[1] * 1e-6) / 1e9
+        return dict(c_us_per_req=coef[0], d_us_per_kv_token=coef[1], e_us=coef[2], r2=r2,
+                    mae_us=mae, implied_kv_gbs=bw, points=len(sel))
+
+    fit = fit_of("us_step")
+    fit_graph = fit_of("us_step_graph")
     with open(os.path.join(outdir, "decode_latency_surface_fit.json"), "w") as f:
-        json.dump(fit, f, indent=1)
-    print(json.dumps({"surface_points": len(rows), "fit": fit}), flush=True)
+        json.dump({"eager": fit, "graph": fit_graph}, f, indent=1)
+    print(json.dumps({"surface_points": len(rows), "fit": fit, "fit_graph": fit_graph}), flush=True)
 
 
 GEMM_SHAPES = (("qkv", 6144, 4096), ("o_proj", 4096, 4096), ("gate_up", 28672, 4096),

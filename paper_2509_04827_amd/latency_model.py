@@ -41,14 +41,16 @@ class LinearFit:
         return kv_bytes_per_token / (self.d * 1e-6) / 1e9
 
 
-def load_surface(path: str, n_q_heads: int | None = 32):
-    """Rows of a latency-surface CSV as (n_req, n_kv, us_step) arrays."""
+def load_surface(path: str, n_q_heads: int | None = 32, column: str = "us_step"):
+    """Rows of a latency-surface CSV as (n_req, n_kv, step time) arrays;
+    `column` picks the eager step time (us_step) or the graph replay time
+    (us_step_graph)."""
     with open(path) as f:
         rows = [r for r in csv.DictReader(f)
                 if n_q_heads is None or int(r["n_q_heads"]) == n_q_heads]
     n_req = np.array([int(r["n_req"]) for r in rows], float)
     n_kv = np.array([int(r["n_kv"]) for r in rows], float)
-    t = np.array([float(r["us_step"]) for r in rows], float)
+    t = np.array([float(r[column]) for r in rows], float)
     return n_req, n_kv, t
 
 

@@ -335,6 +335,48 @@ def test_staged_plan_once_two_layers():
     assert torch.equal(outs[0].view(torch.int32).cpu(), fused.view(torch.int32).cpu())
 
 
+def test_hip_graph_replay():
+    """A whole step (plan, attention, combine kernels) captured into a HIP
+    graph: every replay, with eager work and a synchronisation between
+    replays, equals the eager result bit for bit, and a replay after new Q
+    values are written in place gives the new eager result."""
+    say("case: HIP graph capture and replay of vd_decode_attn")
+    c = custom([37, 700, 4100, 1, 260], seed=19)
+    d = dev_case(c)
+    maxp = c["max_pages_per_seq"]
+    ws = vd.alloc_workspace(5, 32, 8, maxp)
+
+    def step(out):
+        vd.vd_decode_attn(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"], out,
+                          d["scale"], ws)
+
+    eager = torch.empty(d["q"].shape, dtype=torch.float32, device=DEV)
+    step(eager)
+    out = torch.empty_like(eager)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step(out)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step(out)
+    for i in range(4):
+        out.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int32), eager.view(torch.int32)), "replay %d" % i
+    check_f32(out, ref_of(c), "graph replay")
+    gen = torch.Generator(device="cpu").manual_seed(20)
+    d["q"].copy_(torch.randn(d["q"].shape, generator=gen).to(torch.bfloat16))
+    step(eager)
+    out.fill_(float("nan"))
+    g.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int32), eager.view(torch.int32)), "replay with new Q"
+
+
 # ------------------------------------------------------------------ randomized sweep
 @pytest.mark.parametrize("trial", range(12))
 def test_random_shapes(trial):
