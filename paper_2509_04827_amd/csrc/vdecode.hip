@@ -71,7 +71,8 @@ constexpr int kMinRangeTiles = 4;      // small steps: at least this many tiles 
 constexpr int kMaxResidentGroups = 4096;
 constexpr int kPlanThreads = 1024;
 constexpr int kHeadsPerGroup = 4;      // preferred KV heads (waves) per attention workgroup
-constexpr int kAttnGroupsPerCU = 1;    // resident attention workgroups per CU
+constexpr int kAttnWavesPerCU = 4;     // resident attention waves per CU (one per SIMD)
+constexpr int kDeferEntries = 64;      // LDS result entries per wave, over G query heads
 constexpr int kAttnMaxThreads = 64 * kHeadsPerGroup;
 constexpr int kCombineThreads = 256;
 constexpr int kCombineGroupsPerCU = 4;
@@ -732,11 +733,15 @@ attn_kernel(const AttnArgs a)
         }
     } else {
         // Per wave: up to kDefer piece results, written out when the wave's
-        // work is done (or when all entries are taken).
-        constexpr int kDefer = 64 / G;
-        __shared__ float s_res[kHeadsPerGroup][kDefer][G * kHeadDim];
-        __shared__ float2 s_ml[kHeadsPerGroup][kDefer][G];
-        __shared__ int2 s_meta[kHeadsPerGroup][kDefer];   // {whole, out row or partial slot}
+        // work is done (or when all entries are taken).  Dynamic LDS, sized
+        // for the workgroup's HW waves (attn_lds_bytes).
+        constexpr int kDefer = kDeferEntries / G;
+        extern __shared__ __attribute__((aligned(16))) char s_dyn[];
+        float (*s_res)[kDefer][G * kHeadDim] = (float (*)[kDefer][G * kHeadDim])s_dyn;
+        float2 (*s_ml)[kDefer][G] =
+            (float2 (*)[kDefer][G])(s_dyn + (size_t)HW * kDefer * G * kHeadDim * sizeof(float));
+        int2 (*s_meta)[kDefer] =    // {whole, out row or partial slot}
+            (int2 (*)[kDefer])(s_dyn + (size_t)HW * kDefer * G * (kHeadDim * sizeof(float) + sizeof(float2)));
         int n_res = 0;
         auto flush = [&]() {
             constexpr int kF32Chunks = G * kHeadDim / 4, kBf16Chunks = G * kHeadDim / 8;
@@ -1111,8 +1116,19 @@ int log2_pow2(int x)
 // not queried yet; concurrent first calls store the same value.
 std::atomic<int> g_resident[kMaxDevices][5][3][3];
 
+// Dynamic LDS of an attention workgroup: per wave, kDeferEntries / G piece
+// results of G x head_dim floats, their (max, normaliser) pairs and a
+// {whole, target} pair each.  The gather keeps nothing in LDS.
+size_t attn_lds_bytes(int G, int mode, int HW)
+{
+    if (mode == MODE_GATHER)
+        return 0;
+    const size_t entries = (size_t)HW * (kDeferEntries / G);
+    return entries * ((size_t)G * kHeadDim * sizeof(float) + G * sizeof(float2) + 2 * sizeof(int));
+}
+
 // Workgroups of the attention kernel (HW waves each) that fit on the device
-// at once.
+// at once, at most kAttnWavesPerCU waves per CU.
 int resident_attn_groups(int G, int mode, int HW, int *groups)
 {
     int dev = 0;
@@ -1137,10 +1153,11 @@ int resident_attn_groups(int G, int mode, int HW, int *groups)
     if (!k)
         return VD_ERROR_NOT_SUPPORTED;
     int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 64 * HW, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 64 * HW,
+                                                     attn_lds_bytes(G, mode, HW)) != hipSuccess ||
         per_cu <= 0)
         return VD_ERROR_LAUNCH;
-    *groups = std::min(cus * std::min(per_cu, kAttnGroupsPerCU), kMaxResidentGroups);
+    *groups = std::min(cus * std::min(per_cu, std::max(1, kAttnWavesPerCU / HW)), kMaxResidentGroups);
     if (slot)
         slot->store(*groups, std::memory_order_relaxed);
     return VD_SUCCESS;
@@ -1171,7 +1188,8 @@ int enqueue_attn(const AttnArgs &args, int G, int mode, hipStream_t stream)
     const void *k = attn_kernel_ptr(G, mode);
     AttnArgs copy = args;
     void *params[] = {(void *)&copy};
-    if (hipLaunchKernel(k, dim3(groups), dim3(64 * args.HW), params, 0, stream) != hipSuccess)
+    if (hipLaunchKernel(k, dim3(groups), dim3(64 * args.HW), params,
+                        attn_lds_bytes(G, mode, args.HW), stream) != hipSuccess)
         return VD_ERROR_LAUNCH;
     return launch_status();
 }
