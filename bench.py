@@ -23,6 +23,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -35,11 +36,20 @@ WORKLOAD = "chat_b256"
 
 
 def kernel_source_hash() -> str:
+    """Hash of the attention library's code (sources and build flags), with
+    comments and whitespace removed, so that counters taken on one build
+    are reported only for the same code."""
     h = hashlib.sha256()
     for rel in ("paper_2509_04827_amd/csrc/vdecode.hip", "include/vdecode.h",
                 "paper_2509_04827_amd/build.py"):
-        with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, rel)) as f:
+            text = f.read()
+        if rel.endswith(".py"):
+            text = re.sub(r"#[^\n]*", "", text)
+        else:
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            text = re.sub(r"//[^\n]*", "", text)
+        h.update("".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

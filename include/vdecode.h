@@ -24,13 +24,19 @@
  *   out        bf16 (default) or fp32 (VD_FLAG_OUT_F32) [num_seqs][n_q_heads][head_dim]
  *
  * Supported shapes: head_dim = 128, page_size = 16,
- * G in {1, 2, 4, 8, 16}, 0 <= num_seqs <= 8192.
+ * G in {1, 2, 4, 8, 16}, 0 <= num_seqs <= 8192, and sizes whose indices fit
+ * 32 bits: n_kv_heads * 2048 < 2^30, num_seqs * (max_pages_per_seq + 1) *
+ * n_kv_heads < 2^31, num_seqs * max_pages_per_seq * 16 < 2^31 and
+ * num_seqs * n_q_heads < 2^31.
  *
  * Conventions for every call:
  *   - Pointers are device pointers owned by the caller; the library never
- *     allocates, frees or synchronises, and keeps no global state, so calls
- *     from several threads are safe.  Concurrent calls need distinct
- *     workspaces.  out must not alias an input.
+ *     allocates, frees or synchronises.  Its only global state is a per-device
+ *     cache of the compute-unit count and the kernels' occupancy, filled on
+ *     first use (atomics), so calls from several threads are safe.
+ *     Concurrent calls need distinct workspaces.  out must not alias an
+ *     input.  A call enqueues kernel launches only, so it can be captured
+ *     into a HIP graph (after one call on the device outside capture).
  *   - q, k_pages, v_pages, out, k_out, v_out and workspace must be 16-byte
  *     aligned; page_table and seq_lens 4-byte aligned.
  *   - Work is enqueued on `stream` and the call returns at once.
@@ -57,7 +63,7 @@ extern "C" {
 typedef enum vd_status {
     VD_SUCCESS = 0,
     VD_ERROR_INVALID_VALUE = 1,       /* NULL pointer, bad size, misalignment, bad flag, non-finite scale */
-    VD_ERROR_NOT_SUPPORTED = 2,       /* head_dim, page_size, G or num_seqs outside the supported set */
+    VD_ERROR_NOT_SUPPORTED = 2,       /* head_dim, page_size, G, num_seqs or a 32-bit size limit outside the supported set */
     VD_ERROR_WORKSPACE_TOO_SMALL = 3, /* workspace_bytes below vd_decode_workspace_size() */
     VD_ERROR_LAUNCH = 4               /* a kernel launch failed (hipGetLastError) */
 } vd_status;
