@@ -10,8 +10,9 @@
 //
 //   * a workgroup owns 16 * NB output columns (NB 16-column MFMA blocks: 1
 //     for batches up to 8 rows, 4 above, where the x rows are re-read less
-//     often) and a slice of K; its four waves take a quarter of the slice
-//     each and merge their accumulators in LDS in a fixed order;
+//     often) and a slice of K; its four waves (eight when 16-column tiles
+//     number at most one per CU) split the slice and merge their
+//     accumulators in LDS in a fixed order;
 //   * a wave loads the weight rows in whole 128-byte pieces (8 rows per
 //     instruction, 8 lanes per row) and moves them through its own LDS tile
 //     into the B operand of v_mfma_f32_16x16x32_bf16 (lane = output column):
@@ -39,12 +40,11 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kGemmThreads = 256;             // four waves split the K slice
 constexpr int kTileN = 64;                    // column granularity of N (the widest tile)
 constexpr int kKStep = 32;                    // K per MFMA
 constexpr int kUnroll = 4;                    // K steps per load batch (the LDS tile assumes 4)
 constexpr int kBatchK = kKStep * kUnroll;     // 128
-constexpr int kSliceAlign = 4 * kBatchK;      // K slice granularity: 512
+constexpr int kSliceAlign = 4 * kBatchK;      // K slice granularity: 512 (four waves x one batch)
 constexpr int kMaxM = 64;
 constexpr int kReduceThreads = 256;
 constexpr int kGemmGroupsPerCU = 1;           // split K until this many workgroups exist
@@ -67,21 +67,23 @@ __device__ inline unsigned short bf16_rne(float f)
     return __builtin_bit_cast(unsigned short, (__bf16)f);
 }
 
-template <int NB, int MB, int MODE>   // MODE 0: bf16 y, 1: fp32 y, 2: fp32 partial per K slice
-__global__ void __launch_bounds__(kGemmThreads)
+// MODE 0: bf16 y, 1: fp32 y, 2: fp32 partial per K slice.  WAVES waves split
+// the K slice (4, or 8 when there are few column tiles).
+template <int NB, int MB, int MODE, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES)
 gemm_kernel(const GemmArgs a)
 {
     constexpr int kNB = NB;
-    __shared__ f32x4 red[3][kNB * MB][64];
+    __shared__ f32x4 red[WAVES - 1][kNB * MB][64];
     // per wave: the batch's weight rows, 16 rows x 256 B (+16 B against bank
     // conflicts on the column reads) per block
     static_assert(kUnroll == 4, "two row halves x two K halves per block");
-    __shared__ u32x4 wst[4][kNB][16][4 * kUnroll + 1];
+    __shared__ u32x4 wst[WAVES][kNB][16][4 * kUnroll + 1];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int r = lane & 15, grp = lane >> 4;
     const int n0 = blockIdx.x * 16 * kNB;
     const int slice = blockIdx.y;
-    const int kw = a.kslice / 4;
+    const int kw = a.kslice / WAVES;
     const int kb = slice * a.kslice + wave * kw;
     const int K = a.K, M = a.M;
 
@@ -161,7 +163,7 @@ gemm_kernel(const GemmArgs a)
     if (nbatch & 1)
         compute(b0);
 
-    // merge the four waves in order 0, 1, 2, 3
+    // merge the waves in order 0, 1, ..., WAVES - 1
     if (wave > 0) {
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb)
@@ -177,9 +179,9 @@ gemm_kernel(const GemmArgs a)
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
             f32x4 v = acc[nb][mb];
-            v += red[0][nb * MB + mb][lane];
-            v += red[1][nb * MB + mb][lane];
-            v += red[2][nb * MB + mb][lane];
+#pragma unroll
+            for (int x = 0; x < WAVES - 1; ++x)
+                v += red[x][nb * MB + mb][lane];
             // v[i]: row 16mb + 4grp + i, column n0 + 16nb + r
             const int n = n0 + 16 * nb + r;
 #pragma unroll
@@ -273,16 +275,24 @@ int gemm_slices(int M, int N, int K, int cus)
     return S;
 }
 
-template <int NB, int MB>
+// Waves per workgroup: 8 for 16-column tiles when they number at most one per
+// CU (more K parallelism per tile: down and o_proj at small M), if the K
+// slice is whole 8-wave batches; else 4.
+int gemm_waves(int M, int N, int K, int S, int cus)
+{
+    return gemm_nb(M) == 1 && N / 16 <= cus && (K / S) % (8 * kBatchK) == 0 ? 8 : 4;
+}
+
+template <int NB, int MB, int WAVES>
 void launch_gemm(const GemmArgs &g, int S, bool f32, hipStream_t stream)
 {
-    const dim3 grid(g.N / (16 * NB), S);
+    const dim3 grid(g.N / (16 * NB), S), block(64 * WAVES);
     if (S > 1)
-        hipLaunchKernelGGL((gemm_kernel<NB, MB, 2>), grid, dim3(kGemmThreads), 0, stream, g);
+        hipLaunchKernelGGL((gemm_kernel<NB, MB, 2, WAVES>), grid, block, 0, stream, g);
     else if (f32)
-        hipLaunchKernelGGL((gemm_kernel<NB, MB, 1>), grid, dim3(kGemmThreads), 0, stream, g);
+        hipLaunchKernelGGL((gemm_kernel<NB, MB, 1, WAVES>), grid, block, 0, stream, g);
     else
-        hipLaunchKernelGGL((gemm_kernel<NB, MB, 0>), grid, dim3(kGemmThreads), 0, stream, g);
+        hipLaunchKernelGGL((gemm_kernel<NB, MB, 0, WAVES>), grid, block, 0, stream, g);
 }
 
 }  // namespace
@@ -326,13 +336,16 @@ int vd_gemm_bf16(const void *x, const void *w, void *y, int M, int N, int K, voi
     g.kslice = K / S;
     const bool f32 = flags & VD_FLAG_OUT_F32;
     if (gemm_nb(M) == 1) {
-        launch_gemm<1, 1>(g, S, f32, stream);
+        if (gemm_waves(M, N, K, S, cus) == 8)
+            launch_gemm<1, 1, 8>(g, S, f32, stream);
+        else
+            launch_gemm<1, 1, 4>(g, S, f32, stream);
     } else {
         switch ((M + 15) / 16) {
-        case 1: launch_gemm<4, 1>(g, S, f32, stream); break;
-        case 2: launch_gemm<4, 2>(g, S, f32, stream); break;
-        case 3: launch_gemm<4, 3>(g, S, f32, stream); break;
-        default: launch_gemm<4, 4>(g, S, f32, stream); break;
+        case 1: launch_gemm<4, 1, 4>(g, S, f32, stream); break;
+        case 2: launch_gemm<4, 2, 4>(g, S, f32, stream); break;
+        case 3: launch_gemm<4, 3, 4>(g, S, f32, stream); break;
+        default: launch_gemm<4, 4, 4>(g, S, f32, stream); break;
         }
     }
     if (S > 1) {

@@ -19,8 +19,11 @@ from workloads import bits
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 
+# 8-wave workgroups: (1, 4096, 4096), (3, 4096, 14336) and, with K split over
+# two workgroups, (4, 2048, 2048); the others take four waves
 SHAPES = [(1, 4096, 4096), (7, 6144, 4096), (9, 4096, 4096), (16, 512, 512),
-          (33, 1024, 14336), (48, 4096, 14336), (64, 28672, 4096), (64, 64, 512), (17, 128, 1024)]
+          (33, 1024, 14336), (48, 4096, 14336), (64, 28672, 4096), (64, 64, 512), (17, 128, 1024),
+          (3, 4096, 14336), (4, 2048, 2048)]
 
 
 def inputs(M, N, K, seed):
