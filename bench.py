@@ -1,6 +1,7 @@
 """Decode-attention benchmark on one MI355X.
 
-One step = one whole decode-attention call (plan + attention + combine) over
+One step = one whole decode-attention call (self-planned attention kernel +
+combine kernel) over
 the chat-like batch: 256 requests, 32 query / 8 KV heads, head_dim 128,
 lengths lognormal (median 1200, sigma 0.8) clipped to [16, 16384], 16-token
 pages in shuffled order, bf16 N(0,1) values, seed 0 (synthetic; stands in for
@@ -117,9 +118,9 @@ def latency_surface(outdir: str, iters: int = 10, warmup: int = 3):
             if e0 is None:
                 vd.vd_decode_attn(q, kp, vp, ptd, sl, out, scale, ws, stream=stream)
                 return
-            vd.vd_decode_plan(sl, Hq, Hkv, maxp, ws, stream=stream)
             e0.record(stream)
-            vd.vd_decode_partial(q, kp, vp, ptd, sl, out, scale, ws, stream=stream)
+            vd.vd_decode_partial(q, kp, vp, ptd, sl, out, scale, ws, flags=vd.VD_FLAG_SELF_PLAN,
+                                 stream=stream)
             e1.record(stream)
             vd.vd_decode_combine(out, Hkv, maxp, ws, stream=stream)
 
@@ -337,14 +338,15 @@ def main():
     torch.cuda.synchronize()
 
     def step(ev0=None, ev1=None):
-        # one call, three kernels (plan, attention, combine); with events,
-        # the same three stages called one by one around the attention launch
+        # one call, two kernels (self-planned attention, combine); with
+        # events, the same two stages called one by one around the attention
+        # launch
         if ev0 is None:
             vd.vd_decode_attn(q, k, v, pt, sl, out, c["scale"], ws, stream=stream)
             return
-        vd.vd_decode_plan(sl, Hq, Hkv, maxp, ws, stream=stream)
         ev0.record(stream)
-        vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws, stream=stream)
+        vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws, flags=vd.VD_FLAG_SELF_PLAN,
+                             stream=stream)
         ev1.record(stream)
         vd.vd_decode_combine(out, Hkv, maxp, ws, stream=stream)
 

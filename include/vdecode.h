@@ -70,6 +70,10 @@ typedef enum vd_status {
 
 /* flags */
 #define VD_FLAG_OUT_F32 (1u << 0)     /* out is fp32 instead of bf16 */
+/* vd_decode_partial plans the step itself, inside the attention kernel, and
+ * needs no vd_decode_plan before it; ignored by the other calls
+ * (vd_decode_attn always plans this way). */
+#define VD_FLAG_SELF_PLAN (1u << 1)
 /* bits 8..15: cut the step's (page, KV head) tiles into ranges of this many
  * tiles (1..255) instead of the automatic partition (0).  Changes where the
  * split-K boundaries fall, not the result beyond rounding; for tests.  The
@@ -95,8 +99,10 @@ size_t vd_decode_workspace_size(int num_seqs, int n_q_heads, int n_kv_heads,
                                 int max_pages_per_seq, unsigned flags);
 
 /*
- * The whole decode-attention step: vd_decode_plan, vd_decode_partial and
- * vd_decode_combine enqueued back to back on `stream`.
+ * The whole decode-attention step, two kernels enqueued on `stream`: the
+ * attention kernel, planning the step itself (vd_decode_partial with
+ * VD_FLAG_SELF_PLAN), then the combine kernel (vd_decode_combine).  The
+ * result equals that of the staged calls bit for bit.
  * scale: the softmax scale applied to q.k (1/sqrt(head_dim) for standard
  * attention); must be finite.
  */
@@ -113,6 +119,8 @@ int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
  * device runs waves at once, so every wave streams the same number of tiles
  * whatever the length mix; write that plan into the workspace.  Depends only
  * on seq_lens and the sizes, so one plan serves every layer of a decode step.
+ * Not needed before a vd_decode_partial with VD_FLAG_SELF_PLAN, which cuts
+ * the same ranges itself.
  */
 int vd_decode_plan(const int32_t *seq_lens, int num_seqs, int n_q_heads,
                    int n_kv_heads, int head_dim, int page_size,
@@ -125,7 +133,10 @@ int vd_decode_plan(const int32_t *seq_lens, int num_seqs, int n_q_heads,
  * here; the others leave one partial per range they touch in the workspace.
  * Arguments as vd_decode_attn; seq_lens, the sizes and flags must match the
  * plan's.  Several calls may follow one plan (one per layer), each finished
- * by vd_decode_combine before the next reuses the workspace.
+ * by vd_decode_combine before the next reuses the workspace.  With
+ * VD_FLAG_SELF_PLAN the kernel plans from seq_lens itself and writes what
+ * vd_decode_combine reads; the plan in the workspace is then neither read
+ * nor needed.
  */
 int vd_decode_partial(const void *q, const void *k_pages, const void *v_pages,
                       const int32_t *page_table, const int32_t *seq_lens,
@@ -137,7 +148,8 @@ int vd_decode_partial(const void *q, const void *k_pages, const void *v_pages,
 
 /*
  * Stage 3 of 3: log-sum-exp merge of the partials of every request that was
- * split, and zeros for requests with L_b = 0.  Sizes and flags as the plan's.
+ * split, and zeros for requests with L_b = 0.  Sizes and flags as the
+ * preceding vd_decode_partial's.
  */
 int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads,
                       int head_dim, int page_size, int max_pages_per_seq,

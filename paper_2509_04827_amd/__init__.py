@@ -33,6 +33,7 @@ VD_ERROR_NOT_SUPPORTED = 2
 VD_ERROR_WORKSPACE_TOO_SMALL = 3
 VD_ERROR_LAUNCH = 4
 VD_FLAG_OUT_F32 = 1 << 0
+VD_FLAG_SELF_PLAN = 1 << 1
 VD_FLAG_RANGE_SHIFT = 8
 
 EXPORTS = ("vd_status_string", "vd_decode_workspace_size", "vd_decode_attn", "vd_decode_plan",

@@ -12,7 +12,7 @@
 // HW head rows (HW x 256 B, contiguous in the token-major page) at about the
 // same time.  A "tile" is one 16-token page of one head group.  All tiles of
 // the step are laid out in one sequence, ordered by (request b, head group
-// q, page j); a "segment" is the run of tiles of one (b, q).  The planner
+// q, page j); a "segment" is the run of tiles of one (b, q).  The plan
 // cuts the sequence into W ranges of equal length (W a multiple of the
 // number of resident workgroups: four waves per CU), so every workgroup
 // streams the same number of tiles whatever the length mix.  A range may end inside a segment and
@@ -23,12 +23,19 @@
 // them without collisions; a head's partial slot is that times HW plus its
 // index in the group.
 //
-// Three kernels on the caller's stream:
+// Kernels on the caller's stream.  The whole step (vd_decode_attn) is two:
+// a self-planned attention kernel and the combine kernel.  The staged API
+// runs the planner first, once per step, and a planned attention kernel per
+// layer.
 //   plan_kernel     one workgroup: tile offsets per request, range starts,
-//                   and the list of segments to merge (first partial slot,
-//                   number of pieces).
-//   attn_kernel     one workgroup per range (grid-stride over ranges), one
-//                   wave per KV head of the group.  Per page:
+//                   a boundary record per range (which segment a range
+//                   boundary cuts: its first partial slot and piece count),
+//                   and the list of requests without tokens.
+//   attn_kernel     R resident workgroups, each taking consecutive ranges,
+//                   one wave per KV head of the group.  Self-planned, each
+//                   workgroup first scans the request lengths in LDS to find
+//                   its ranges' start and boundary records (the planner's
+//                   arithmetic, so both cut identical ranges).  Per page:
 //                     K rows are loaded straight into MFMA A operands (lane =
 //                     token row); scores = K Q^T with v_mfma_f32_16x16x32_bf16
 //                     against the group's G query heads (columns past G
@@ -40,14 +47,16 @@
 //                     v_mfma_f32_16x16x16_bf16, whose B operand is P exactly
 //                     as the score MFMA left it (P split into bf16 hi + lo).
 //                   A wave's K/V stream runs on across pieces: the next
-//                   piece's descriptor comes from scalar loads, its page ids
+//                   piece's bounds come from scalar loads of request
+//                   lengths, its page ids
 //                   and Q are loaded a piece ahead, and its first page while
 //                   the current piece's last page is consumed.  Piece results
 //                   wait in LDS (up to 64 / G per wave) and are written when
 //                   the wave's work is done, so no stores interleave with the
 //                   stream.
-//   combine_kernel  log-sum-exp merge of each listed segment's partials
-//                   (zeros for requests without tokens).
+//   combine_kernel  log-sum-exp merge of the partials of each segment that
+//                   a range boundary cuts (zeros for requests without
+//                   tokens).
 //
 // All arithmetic is fp32; bf16 is only the storage type of Q/K/V, the MFMA
 // operand type, and the optional output type.
@@ -91,14 +100,14 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 struct PlanHeader {
     int n_ranges;  // W
     int n_tiles;   // T
-    int n_short;   // merge-list entries with at most kShortMerge pieces (front of the list)
-    int n_long;    // entries with more pieces (back of the list)
-    int pad[4];
+    int n_empty;   // requests without tokens (listed for the combine kernel)
+    int pad[5];
 };
 
 // ---------------------------------------------------------------- workspace
 struct WsLayout {
-    size_t hdr, tok_base, merge, ranges, part_ml, part_acc, total;
+    size_t hdr, tok_base, bounds, empty, ranges, part_ml, part_acc, total;
+    long long cap;   // most ranges any plan of these sizes can have
 };
 
 __host__ __device__ inline long long ceil_div_ll(long long a, long long b) { return (a + b - 1) / b; }
@@ -128,10 +137,12 @@ inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced)
     cap = std::max(cap, 1LL);
     const long long slots = cap * HW + (long long)B * Hkv;
     WsLayout l;
+    l.cap = cap;
     size_t o = 0;
     l.hdr = o;       o = align_up(o + sizeof(PlanHeader), 256);
     l.tok_base = o;  o = align_up(o + sizeof(long long) * (size_t)(B + 1), 256);
-    l.merge = o;     o = align_up(o + sizeof(int4) * (size_t)B * (Hkv / HW), 256);
+    l.bounds = o;    o = align_up(o + sizeof(int4) * (size_t)cap, 256);
+    l.empty = o;     o = align_up(o + sizeof(int) * (size_t)B, 256);
     l.ranges = o;    o = align_up(o + sizeof(int4) * (size_t)(cap + 1), 256);
     l.part_ml = o;   o = align_up(o + sizeof(float2) * (size_t)slots * G, 256);
     l.part_acc = o;  o = align_up(o + sizeof(float) * (size_t)slots * G * kHeadDim, 256);
@@ -139,9 +150,11 @@ inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced)
     return l;
 }
 
-// ---------------------------------------------------------------- planner
+// ---------------------------------------------------------------- planning
+// The same arithmetic serves the planner kernel (staged API) and the
+// attention kernel's own prologue (whole step), so both cut identical ranges.
 constexpr int kPlanPerThread = kMaxSeqs / kPlanThreads;   // requests per planner thread
-constexpr int kShortMerge = 8;         // merge entries with more pieces take the piece-lane path
+constexpr int kShortMerge = 8;         // segments with more pieces are merged per query head
 
 __device__ inline int clamped_len(const int32_t *seq_lens, int b, int maxp)
 {
@@ -149,10 +162,76 @@ __device__ inline int clamped_len(const int32_t *seq_lens, int b, int maxp)
     return L <= 0 ? 0 : min(L, maxp * kPage);
 }
 
-// range holding tile t when range w starts at floor(w * T / W)
+// Number of ranges W for T tiles in nseg non-empty segments.  A forced
+// length c gives ceil(T / c).  Otherwise ranges hold at least m tiles, m the
+// mean segment length clamped to [1, kMinRangeTiles] (so short segments go
+// one to a range rather than several in a row), up to R ranges; past that W
+// is a multiple of R with at most kMaxRangeTiles tiles per range.  W <= T,
+// so no range is empty.
+__device__ inline int plan_ranges(int T, int nseg, int forced, int R)
+{
+    if (T == 0)
+        return 0;
+    if (forced > 0)
+        return (int)ceil_div_ll(T, forced);
+    const int m = (int)std::min<long long>(kMinRangeTiles, ceil_div_ll(T, std::max(nseg, 1)));
+    const long long W = std::min<long long>(R, ceil_div_ll(T, m));
+    return W == R ? (int)(R * ceil_div_ll(T, (long long)kMaxRangeTiles * R)) : (int)W;
+}
+
+// first tile of range w: floor(w * T / W)
+__device__ inline int range_start(int w, int T, int W) { return (int)((long long)w * T / W); }
+
+// range holding tile t
 __device__ inline int range_of(long long t, long long T, long long W)
 {
     return (int)(((t + 1) * W - 1) / T);
+}
+
+// Ranges [lo, hi) of workgroup g of n: consecutive, as equal in number as
+// they can be.
+__device__ inline int2 group_ranges(int g, int n, int W)
+{
+    return make_int2((int)((long long)g * W / n), (int)((long long)(g + 1) * W / n));
+}
+
+// Boundary record of range w >= 1, whose first tile t is page j of segment
+// s (P pages): {s, first partial slot of s, pieces of s, index of this
+// boundary among those inside s}.  A range that starts a segment (j = 0)
+// gets pieces = 0: nothing to merge there.  The combine kernel reads one
+// record per boundary.
+__device__ inline int4 boundary_record(int w, int t, int s, int j, int P, int T, int W)
+{
+    if (j == 0)
+        return make_int4(s, 0, 0, 0);
+    const int first = t - j;
+    const int w0 = range_of(first, T, W), w1 = range_of(first + P - 1, T, W);
+    return make_int4(s, w0 + s, w1 - w0 + 1, w - w0 - 1);
+}
+
+// Largest b in [0, B) with pre[b] <= t (pre ascending, pre[B] = T > t): the
+// request holding tile t.
+__device__ inline int find_request(const int *pre, int B, int t)
+{
+    int lo = 0, hi = B;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (pre[mid] <= t) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
+// Descriptor {b, q, j, t} of range w's first tile, and its boundary record.
+__device__ inline void range_entry(const int *pre, int B, int Hg, int w, int T, int W, int4 &desc,
+                                   int4 &rec)
+{
+    const int t = range_start(w, T, W);
+    const int b = find_request(pre, B, t);
+    const int P = (pre[b + 1] - pre[b]) / Hg;
+    const int off = t - pre[b];
+    const int q = off / P, j = off - q * P;
+    desc = make_int4(b, q, j, t);
+    rec = boundary_record(w, t, b * Hg + q, j, P, T, W);
 }
 
 template <typename T>
@@ -177,7 +256,7 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
     __shared__ int s_pre[kMaxSeqs + 1];
     __shared__ int s_wtiles[kPlanThreads / 64];
     __shared__ long long s_wtok[kPlanThreads / 64];
-    __shared__ int s_W, s_T, s_nshort, s_nlong;
+    __shared__ int s_nempty;
     const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
     const int per = (B + kPlanThreads - 1) / kPlanThreads;
     const int b0 = t * per;
@@ -200,10 +279,8 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
         s_wtiles[wv] = inc_tiles;
         s_wtok[wv] = inc_tok;
     }
-    if (t == 0) {
-        s_nshort = 0;
-        s_nlong = 0;
-    }
+    if (t == 0)
+        s_nempty = 0;
     __syncthreads();
     int base_tiles = 0;
     long long base_tok = 0;
@@ -214,84 +291,48 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
     int pre = base_tiles + inc_tiles - my_tiles;
     long long tpre = base_tok + inc_tok - my_tok;
     long long *tok_base = (long long *)(ws + lay.tok_base);
+    int *empty = (int *)(ws + lay.empty);
 #pragma unroll
     for (int k = 0; k < kPlanPerThread; ++k) {
         const int b = b0 + k;
         if (k < per && b < B) {
             s_pre[b] = pre;
             tok_base[b] = tpre;
+            if (tiles[k] == 0)
+                empty[atomicAdd(&s_nempty, 1)] = b;
         }
         pre += tiles[k];
         tpre += lens[k];
     }
     if (t == kPlanThreads - 1) {
         // the last thread's running sums are the totals
-        const int T = pre;
-        s_pre[B] = T;
+        s_pre[B] = pre;
         tok_base[B] = tpre;
-        long long W;
-        if (T == 0) {
-            W = 0;
-        } else if (forced > 0) {
-            W = ceil_div_ll(T, forced);
-        } else {
-            const long long R = resident_groups;
-            W = std::min<long long>(R, ceil_div_ll(T, kMinRangeTiles));
-            if (W == R)
-                W = R * ceil_div_ll(T, (long long)kMaxRangeTiles * R);
-        }
-        s_W = (int)W;
-        s_T = T;
     }
     __syncthreads();
-    const int W = s_W, T = s_T;
+    const int T = s_pre[B];
+    const int W = plan_ranges(T, (B - s_nempty) * Hg, forced, resident_groups);
 
-    // range starts {b, q, j, t}; range W is the end sentinel
+    // range starts {b, q, j, t} (range W is the end sentinel) and the
+    // boundary records of ranges 1 .. W-1
     int4 *ranges = (int4 *)(ws + lay.ranges);
+    int4 *bounds = (int4 *)(ws + lay.bounds);
     for (int w = t; w <= W; w += kPlanThreads) {
-        const long long tt = W ? (long long)w * T / W : 0;
-        if (tt >= T) {
+        if (w == W) {
             ranges[w] = make_int4(B, 0, 0, T);
             continue;
         }
-        int lo = 0, hi = B;   // largest b with s_pre[b] <= tt
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (s_pre[mid] <= tt) lo = mid; else hi = mid;
-        }
-        const int P = (s_pre[lo + 1] - s_pre[lo]) / Hg;
-        const int off = (int)(tt - s_pre[lo]);
-        ranges[w] = make_int4(lo, off / P, off % P, (int)tt);
+        int4 desc, rec;
+        range_entry(s_pre, B, Hg, w, T, W, desc, rec);
+        ranges[w] = desc;
+        if (w > 0)
+            bounds[w] = rec;
     }
-
-    // per segment: first partial slot and number of pieces; segments with
-    // other than exactly one piece (split, or empty request) go on the merge
-    // list for the combine kernel: up to kShortMerge pieces from the front,
-    // more from the back
-    int4 *merge = (int4 *)(ws + lay.merge);
-    for (int s = t; s < B * Hg; s += kPlanThreads) {
-        const int b = s / Hg, q = s - (s / Hg) * Hg;
-        const int P = (s_pre[b + 1] - s_pre[b]) / Hg;
-        int2 e = make_int2(0, 0);
-        if (P > 0) {
-            const long long t0 = s_pre[b] + (long long)q * P, t1 = t0 + P - 1;
-            const int w0 = range_of(t0, T, W), w1 = range_of(t1, T, W);
-            e = make_int2(w0 + s, w1 - w0 + 1);
-        }
-        if (e.y != 1) {
-            if (e.y <= kShortMerge)
-                merge[atomicAdd(&s_nshort, 1)] = make_int4(b, q, e.x, e.y);
-            else
-                merge[B * Hg - 1 - atomicAdd(&s_nlong, 1)] = make_int4(b, q, e.x, e.y);
-        }
-    }
-    __syncthreads();
     if (t == 0) {
         PlanHeader *h = (PlanHeader *)(ws + lay.hdr);
         h->n_ranges = W;
         h->n_tiles = T;
-        h->n_short = s_nshort;
-        h->n_long = s_nlong;
+        h->n_empty = s_nempty;   // final: every append happened before the barrier
     }
 }
 
@@ -300,12 +341,15 @@ struct AttnArgs {
     const uint16_t *q, *k, *v;
     const int32_t *pt, *seq_lens;
     void *out, *out2;               // attention: out; gather: k_out, v_out
-    const PlanHeader *hdr;
-    const int4 *ranges;
+    PlanHeader *hdr;                // read (planned) or written (self-planned)
+    const int4 *ranges;             // planned only
+    int4 *bounds;                   // self-planned: boundary records written here
+    int *empty;                     // self-planned: requests without tokens
     const long long *tok_base;
     float2 *part_ml;
     float *part_acc;
     int Hq, Hkv, HW, pt_stride, maxp;
+    int B, forced, resident;        // self-planned: requests, forced range length, R
     float scale_log2;
 };
 
@@ -441,25 +485,21 @@ struct Piece {
     int b, q, jb, je, L, w;
 };
 
-// Walks the ranges of one workgroup (blockIdx.x, + gridDim.x, ...) and the
-// pieces each range covers, in order.
+// Walks the ranges [w, w_end) of one workgroup and the pieces each covers,
+// in order.  The ranges are consecutive, so the walk runs on from one into
+// the next: a piece cut by a range end resumes at the next page.
 struct PieceWalk {
-    int w, t_end, b, q, j, t;
+    int w, w_end, T, W;
+    int b, q, j, t, t_end;   // next tile: page j of head group q of request b
 
-    __device__ inline bool next(const AttnArgs &a, int W, int Hg, Piece &p)
+    __device__ inline bool next(const AttnArgs &a, int Hg, Piece &p)
     {
-        const const_i32p ranges = (const_i32p)a.ranges;   // {b, q, j, t} per range
         const const_i32p lens = (const_i32p)a.seq_lens;
         while (true) {
             if (t >= t_end) {
-                w += gridDim.x;
-                if (w >= W)
+                if (++w >= w_end)
                     return false;
-                b = ranges[4 * w];
-                q = ranges[4 * w + 1];
-                j = ranges[4 * w + 2];
-                t = ranges[4 * w + 3];
-                t_end = ranges[4 * w + 7];
+                t_end = range_start(w + 1, T, W);
                 continue;
             }
             const int L = min(lens[b], a.maxp * kPage);
@@ -471,15 +511,96 @@ struct PieceWalk {
             const int n = min(P - j, t_end - t);
             p = Piece{b, q, j, j + n, L, w};
             t += n;
-            j = 0;
-            if (++q == Hg) {
-                q = 0;
-                ++b;
+            if (j + n < P) {
+                j += n;
+            } else {
+                j = 0;
+                if (++q == Hg) {
+                    q = 0;
+                    ++b;
+                }
             }
             return true;
         }
     }
 };
+
+// Self-planned prologue of the attention kernel (whole step, no planner
+// kernel): the workgroup reads every request length and forms the tile
+// prefix in LDS (in the result-entry space, not yet in use); from it come its
+// own ranges' first tile and their boundary records.  Workgroup 0 also writes
+// the header and the list of requests without tokens for the combine kernel.
+// Returns false when the workgroup has no range.
+__device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWalk &walk)
+{
+    __shared__ long long s_wsum[kHeadsPerGroup];
+    __shared__ int4 s_desc;
+    const int nt = blockDim.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, nw = nt >> 6;
+    const int B = a.B;
+    for (int b = tid; b < B; b += nt) {
+        const int L = clamped_len(a.seq_lens, b, a.maxp);
+        s_pre[b] = (L + kPage - 1) / kPage * Hg;
+    }
+    __syncthreads();
+    // exclusive prefix of tiles in place; thread tid owns requests [c0, c1).
+    // The scan carries (non-empty requests << 32) + tiles: both sums at once
+    // (tiles < 2^31, so the low half never carries).
+    const int per = (B + nt - 1) / nt;
+    const int c0 = min(B, tid * per), c1 = min(B, c0 + per);
+    long long mine = 0;
+    for (int b = c0; b < c1; ++b)
+        mine += (1LL << 32) * (s_pre[b] > 0) + s_pre[b];
+    const long long inc = wave_inclusive_scan(mine, lane);
+    if (lane == 63)
+        s_wsum[wv] = inc;
+    __syncthreads();
+    long long base = 0, tot = 0;
+    for (int x = 0; x < nw; ++x) {
+        base += x < wv ? s_wsum[x] : 0;
+        tot += s_wsum[x];
+    }
+    const long long excl = base + inc - mine;
+    const int T = (int)(tot & 0xFFFFFFFFLL), nonempty = (int)(tot >> 32);
+    int run = (int)(excl & 0xFFFFFFFFLL);
+    for (int b = c0; b < c1; ++b) {
+        const int n = s_pre[b];
+        s_pre[b] = run;
+        run += n;
+    }
+    if (tid == 0)
+        s_pre[B] = T;
+    __syncthreads();
+
+    const int W = plan_ranges(T, nonempty * Hg, a.forced, a.resident);
+    const int2 wr = group_ranges(blockIdx.x, gridDim.x, W);
+    for (int w = wr.x + tid; w < wr.y; w += nt) {
+        int4 desc, rec;
+        range_entry(s_pre, B, Hg, w, T, W, desc, rec);
+        if (w == wr.x)
+            s_desc = desc;
+        if (w > 0)
+            a.bounds[w] = rec;
+    }
+    if (blockIdx.x == 0) {
+        // header, and the requests without tokens in order: those before c0
+        // number c0 minus the non-empty ones
+        int pos = c0 - (int)(excl >> 32);
+        for (int b = c0; b < c1; ++b)
+            if (s_pre[b + 1] == s_pre[b])
+                a.empty[pos++] = b;
+        if (tid == 0) {
+            a.hdr->n_ranges = W;
+            a.hdr->n_tiles = T;
+            a.hdr->n_empty = B - nonempty;
+        }
+    }
+    __syncthreads();   // s_desc is set; the prefix is no longer read
+    if (wr.x >= wr.y)
+        return false;
+    const int4 d = s_desc;
+    walk = PieceWalk{wr.x, wr.y, T, W, d.x, d.y, d.z, d.w, range_start(wr.x + 1, T, W)};
+    return true;
+}
 
 // Q operand (B of the score MFMA): head column r, d slice 8(4kk+grp).  Columns
 // r >= G repeat head G-1; their results are never stored.
@@ -704,23 +825,35 @@ __device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageI
 // operand are loaded at the start of a piece, and its first page while the
 // piece's last page is consumed, so the K/V stream of a wave runs on across
 // piece boundaries.
-template <int G, int MODE>
+template <int G, int MODE, bool SELF>
 __global__ void __launch_bounds__(kAttnMaxThreads)
 attn_kernel(const AttnArgs a)
 {
     const int lane = threadIdx.x & 63;
     const int hi = threadIdx.x >> 6;          // KV head within the group
-    const int W = a.hdr->n_ranges;
     const int HW = a.HW, Hg = a.Hkv / a.HW;
-    PieceWalk walk{(int)blockIdx.x - (int)gridDim.x, 0, 0, 0, 0, 0};
+    extern __shared__ __attribute__((aligned(16))) char s_dyn[];
+    PieceWalk walk;
+    if constexpr (SELF) {
+        if (!self_plan(a, Hg, (int *)s_dyn, walk))
+            return;
+    } else {
+        const const_i32p hdr = (const const_i32p)a.hdr;
+        const int W = hdr[0], T = hdr[1];
+        const int2 wr = group_ranges(blockIdx.x, gridDim.x, W);
+        if (wr.x >= wr.y)
+            return;
+        const const_i32p rg = (const_i32p)(a.ranges + wr.x);
+        walk = PieceWalk{wr.x, wr.y, T, W, rg[0], rg[1], rg[2], rg[3], range_start(wr.x + 1, T, W)};
+    }
     Piece cur;
-    if (!walk.next(a, W, Hg, cur))
+    if (!walk.next(a, Hg, cur))
         return;
     PageIds ids = load_page_ids(a.pt + (size_t)cur.b * a.pt_stride, cur.jb, cur.je, lane);
     if constexpr (MODE == MODE_GATHER) {
         while (true) {
             Piece nxt;
-            const bool more = walk.next(a, W, Hg, nxt);
+            const bool more = walk.next(a, Hg, nxt);
             if (!more)
                 nxt = cur;
             const PageIds nids =
@@ -736,7 +869,6 @@ attn_kernel(const AttnArgs a)
         // work is done (or when all entries are taken).  Dynamic LDS, sized
         // for the workgroup's HW waves (attn_lds_bytes).
         constexpr int kDefer = kDeferEntries / G;
-        extern __shared__ __attribute__((aligned(16))) char s_dyn[];
         float (*s_res)[kDefer][G * kHeadDim] = (float (*)[kDefer][G * kHeadDim])s_dyn;
         float2 (*s_ml)[kDefer][G] =
             (float2 (*)[kDefer][G])(s_dyn + (size_t)HW * kDefer * G * kHeadDim * sizeof(float));
@@ -797,7 +929,7 @@ attn_kernel(const AttnArgs a)
             PageIds nids;
             u32x4 nq[4];
             auto fetch_next = [&]() {
-                more = walk.next(a, W, Hg, nxt);
+                more = walk.next(a, Hg, nxt);
                 if (!more) {   // last piece: the final prefetch re-reads its last page
                     nxt = cur;
                     nxt.jb = cur.je - 1;
@@ -838,21 +970,25 @@ attn_kernel(const AttnArgs a)
 struct CombineArgs {
     void *out;
     const PlanHeader *hdr;
-    const int4 *merge;      // short entries from the front, long ones from the back
+    const int4 *bounds;     // boundary record per range 1 .. W-1
+    const int *empty;       // requests without tokens
     const float2 *part_ml;
     const float *part_acc;
-    int Hq, Hkv, G, HW, list_len;
+    int Hq, Hkv, G, HW;
 };
 
-// The merge list holds {b, q, first slot, pieces} per segment to merge.
-// Work items, strided over the workgroups:
-//   short entries (<= kShortMerge pieces, incl. 0 for empty requests): one
-//     item per segment; its HW * G query heads x 32 float4 chunks of head_dim
-//     are spread over the threads, each merging all pieces of its chunk with
-//     the loads of a block of pieces issued before use;
-//   long entries: one item per (segment, query head); 32 chunks x
-//     kCombineLanes piece lanes, lane l merging pieces l, l + lanes, ..., then
-//     the lanes' (max, normaliser, accumulator) merged in LDS.
+// Work items, strided over the workgroups: one per range boundary, then one
+// per request without tokens (its output rows are zeros).  A boundary
+// inside a segment names that segment's first partial slot and piece count n
+// and its own index i among the segment's n - 1 inner boundaries:
+//   n <= kShortMerge: the first inner boundary (i = 0) merges the segment;
+//     its HW * G query heads x 32 float4 chunks of head_dim are spread over
+//     the threads, each merging all pieces of its chunk with the loads of a
+//     block of pieces issued before use;
+//   larger n: inner boundary i merges query heads i, i + n - 1, ...; per
+//     head 32 chunks x kCombineLanes piece lanes, lane l merging pieces l,
+//     l + lanes, ..., then the lanes' (max, normaliser, accumulator) merged
+//     in LDS.
 // Merging is a running log-sum-exp in the exp2 domain.
 constexpr int kCombineLanes = kCombineThreads / (kHeadDim / 4);
 constexpr int kCombineUnroll = 4;
@@ -915,26 +1051,34 @@ combine_kernel(const CombineArgs a)
     __shared__ float s_m[kCombineLanes][kHeadDim / 4];
     __shared__ float s_l[kCombineLanes][kHeadDim / 4];
     __shared__ f32x4 s_o[kCombineLanes][kHeadDim / 4];
-    const int n_short = a.hdr->n_short, n_long = a.hdr->n_long;
-    const int G = a.G, HW = a.HW;
+    const int W = a.hdr->n_ranges, n_empty = a.hdr->n_empty;
+    const int G = a.G, HW = a.HW, Hg = a.Hkv / a.HW;
     const int rows = HW * G;
-    const int n_items = n_short + n_long * rows;
-    for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
-        if (item < n_short) {
-            const int4 m = a.merge[item];
-            const int b = m.x, q = m.y, first = m.z, n = m.w;
+    const int n_bounds = W > 1 ? W - 1 : 0;
+    for (int item = blockIdx.x; item < n_bounds + n_empty; item += gridDim.x) {
+        if (item >= n_bounds) {
+            const int b = a.empty[item - n_bounds];
+            for (int u = threadIdx.x; u < a.Hq * (kHeadDim / 4); u += kCombineThreads)
+                store_out<MODE>(a, (size_t)b * a.Hq * kHeadDim + 4 * u, f32x4{0.f, 0.f, 0.f, 0.f});
+            continue;
+        }
+        const int4 rec = a.bounds[item + 1];
+        const int s = rec.x, first = rec.y, n = rec.z, i = rec.w;
+        const int b = s / Hg, q = s - b * Hg;
+        if (n == 0 || (n <= kShortMerge && i != 0))
+            continue;
+        if (n <= kShortMerge) {
             for (int u = threadIdx.x; u < rows * (kHeadDim / 4); u += kCombineThreads) {
                 const int row = u / (kHeadDim / 4), c4 = u - row * (kHeadDim / 4);
                 const int hi = row / G, hh = row - hi * G;
                 Lse r = {-INFINITY, 0.f, {0.f, 0.f, 0.f, 0.f}};
                 lse_pieces(a, r, first, n, 0, 1, hi, hh, c4);
-                const f32x4 o = n > 0 ? r.o * (1.0f / r.l) : r.o;
-                store_out<MODE>(a, ((size_t)b * a.Hq + (q * HW + hi) * G + hh) * kHeadDim + 4 * c4, o);
+                store_out<MODE>(a, ((size_t)b * a.Hq + (q * HW + hi) * G + hh) * kHeadDim + 4 * c4,
+                                r.o * (1.0f / r.l));
             }
-        } else {
-            const int e = (item - n_short) / rows, row = (item - n_short) - e * rows;
-            const int4 m = a.merge[a.list_len - 1 - e];
-            const int b = m.x, q = m.y, first = m.z, n = m.w;
+            continue;
+        }
+        for (int row = i; row < rows; row += n - 1) {
             const int hi = row / G, hh = row - hi * G;
             const int c4 = threadIdx.x & (kHeadDim / 4 - 1);
             const int pl = threadIdx.x / (kHeadDim / 4);
@@ -1041,7 +1185,7 @@ int check_shapes(int num_seqs, int n_q_heads, int n_kv_heads, int head_dim, int 
         return VD_ERROR_INVALID_VALUE;
     if (n_q_heads % n_kv_heads != 0)
         return VD_ERROR_INVALID_VALUE;
-    if (flags & ~(VD_FLAG_OUT_F32 | VD_FLAG_RANGE_MASK))
+    if (flags & ~(VD_FLAG_OUT_F32 | VD_FLAG_SELF_PLAN | VD_FLAG_RANGE_MASK))
         return VD_ERROR_INVALID_VALUE;
     if (head_dim != kHeadDim || page_size != kPage || !supported_g(n_q_heads / n_kv_heads) ||
         num_seqs > kMaxSeqs)
@@ -1086,12 +1230,17 @@ int num_cus(int *out)
     return VD_SUCCESS;
 }
 
-const void *attn_kernel_ptr(int G, int mode)
+// The attention kernel for G, output mode and planning: planned (tables
+// from the planner kernel) or self-planned (whole step).
+const void *attn_kernel_ptr(int G, int mode, bool self)
 {
     if (mode == MODE_GATHER)
-        return (const void *)attn_kernel<1, MODE_GATHER>;
-#define VD_K(g) (mode == MODE_F32 ? (const void *)attn_kernel<g, MODE_F32> \
-                                  : (const void *)attn_kernel<g, MODE_BF16>)
+        return self ? nullptr : (const void *)attn_kernel<1, MODE_GATHER, false>;
+#define VD_K(g)                                                                                \
+    (self ? (mode == MODE_F32 ? (const void *)attn_kernel<g, MODE_F32, true>                  \
+                              : (const void *)attn_kernel<g, MODE_BF16, true>)                \
+          : (mode == MODE_F32 ? (const void *)attn_kernel<g, MODE_F32, false>                 \
+                              : (const void *)attn_kernel<g, MODE_BF16, false>))
     switch (G) {
     case 1: return VD_K(1);
     case 2: return VD_K(2);
@@ -1115,6 +1264,11 @@ int log2_pow2(int x)
 // occupancy query costs more host time than a small step's kernels.  0 means
 // not queried yet; concurrent first calls store the same value.
 std::atomic<int> g_resident[kMaxDevices][5][3][3];
+
+// The self-planned prologue keeps the tile prefix of up to kMaxSeqs requests
+// in the result-entry space of one wave (the smallest case: G = 16).
+static_assert((kDeferEntries / 16) * (16 * kHeadDim * 4 + 16 * 8 + 2 * 4) >= 4 * (kMaxSeqs + 1),
+              "request prefix does not fit the attention kernel's LDS");
 
 // Dynamic LDS of an attention workgroup: per wave, kDeferEntries / G piece
 // results of G x head_dim floats, their (max, normaliser) pairs and a
@@ -1149,14 +1303,19 @@ int resident_attn_groups(int G, int mode, int HW, int *groups)
     int st = num_cus(&cus);
     if (st)
         return st;
-    const void *k = attn_kernel_ptr(G, mode);
-    if (!k)
-        return VD_ERROR_NOT_SUPPORTED;
-    int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k, 64 * HW,
-                                                     attn_lds_bytes(G, mode, HW)) != hipSuccess ||
-        per_cu <= 0)
-        return VD_ERROR_LAUNCH;
+    // planned and self-planned kernels must agree on R (it sets the ranges)
+    int per_cu = kAttnWavesPerCU;
+    for (int self = 0; self < (mode == MODE_GATHER ? 1 : 2); ++self) {
+        const void *k = attn_kernel_ptr(G, mode, self != 0);
+        if (!k)
+            return VD_ERROR_NOT_SUPPORTED;
+        int n = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, k, 64 * HW,
+                                                         attn_lds_bytes(G, mode, HW)) != hipSuccess ||
+            n <= 0)
+            return VD_ERROR_LAUNCH;
+        per_cu = std::min(per_cu, n);
+    }
     *groups = std::min(cus * std::min(per_cu, std::max(1, kAttnWavesPerCU / HW)), kMaxResidentGroups);
     if (slot)
         slot->store(*groups, std::memory_order_relaxed);
@@ -1179,14 +1338,17 @@ int enqueue_plan(const int32_t *seq_lens, int num_seqs, int G, int n_kv_heads,
     return launch_status();
 }
 
-int enqueue_attn(const AttnArgs &args, int G, int mode, hipStream_t stream)
+int enqueue_attn(const AttnArgs &args, int G, int mode, bool self, hipStream_t stream)
 {
     int groups = 0;
     int st = resident_attn_groups(G, mode, args.HW, &groups);
     if (st)
         return st;
-    const void *k = attn_kernel_ptr(G, mode);
+    const void *k = attn_kernel_ptr(G, mode, self);
+    if (!k)
+        return VD_ERROR_NOT_SUPPORTED;
     AttnArgs copy = args;
+    copy.resident = groups;
     void *params[] = {(void *)&copy};
     if (hipLaunchKernel(k, dim3(groups), dim3(64 * args.HW), params,
                         attn_lds_bytes(G, mode, args.HW), stream) != hipSuccess)
@@ -1194,13 +1356,15 @@ int enqueue_attn(const AttnArgs &args, int G, int mode, hipStream_t stream)
     return launch_status();
 }
 
-AttnArgs make_args(const WsLayout &lay, void *workspace, int n_q_heads, int n_kv_heads,
-                   int max_pages_per_seq, float scale)
+AttnArgs make_args(const WsLayout &lay, void *workspace, int num_seqs, int n_q_heads,
+                   int n_kv_heads, int max_pages_per_seq, float scale, unsigned flags)
 {
     char *ws = (char *)workspace;
     AttnArgs a{};
-    a.hdr = (const PlanHeader *)(ws + lay.hdr);
+    a.hdr = (PlanHeader *)(ws + lay.hdr);
     a.ranges = (const int4 *)(ws + lay.ranges);
+    a.bounds = (int4 *)(ws + lay.bounds);
+    a.empty = (int *)(ws + lay.empty);
     a.tok_base = (const long long *)(ws + lay.tok_base);
     a.part_ml = (float2 *)(ws + lay.part_ml);
     a.part_acc = (float *)(ws + lay.part_acc);
@@ -1209,8 +1373,41 @@ AttnArgs make_args(const WsLayout &lay, void *workspace, int n_q_heads, int n_kv
     a.HW = heads_per_group(n_kv_heads);
     a.pt_stride = max_pages_per_seq;
     a.maxp = max_pages_per_seq;
+    a.B = num_seqs;
+    a.forced = forced_tiles(flags);
     a.scale_log2 = scale * kLog2e;
     return a;
+}
+
+// Combine kernel over the workspace's header, boundary records and list of
+// requests without tokens.
+int enqueue_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, const WsLayout &lay,
+                    void *workspace, unsigned flags, hipStream_t stream)
+{
+    char *ws = (char *)workspace;
+    CombineArgs c;
+    c.out = out;
+    c.hdr = (const PlanHeader *)(ws + lay.hdr);
+    c.bounds = (const int4 *)(ws + lay.bounds);
+    c.empty = (const int *)(ws + lay.empty);
+    c.part_ml = (const float2 *)(ws + lay.part_ml);
+    c.part_acc = (const float *)(ws + lay.part_acc);
+    c.Hq = n_q_heads;
+    c.Hkv = n_kv_heads;
+    c.G = n_q_heads / n_kv_heads;
+    c.HW = heads_per_group(n_kv_heads);
+    int cus = 0;
+    const int st = num_cus(&cus);
+    if (st)
+        return st;
+    // work items: fewer than one per range plus one per request
+    const long long items = lay.cap + (long long)num_seqs;
+    const dim3 grid((unsigned)std::min<long long>((long long)cus * kCombineGroupsPerCU, items));
+    if (flags & VD_FLAG_OUT_F32)
+        hipLaunchKernelGGL(combine_kernel<MODE_F32>, grid, dim3(kCombineThreads), 0, stream, c);
+    else
+        hipLaunchKernelGGL(combine_kernel<MODE_BF16>, grid, dim3(kCombineThreads), 0, stream, c);
+    return launch_status();
 }
 
 int check_attn_args(const void *q, const void *k_pages, const void *v_pages,
@@ -1238,6 +1435,26 @@ int check_attn_args(const void *q, const void *k_pages, const void *v_pages,
 }
 
 int out_mode(unsigned flags) { return (flags & VD_FLAG_OUT_F32) ? MODE_F32 : MODE_BF16; }
+
+// The attention kernel on checked arguments: planned (after the planner
+// kernel) or self-planned.
+int enqueue_partial(const void *q, const void *k_pages, const void *v_pages,
+                    const int32_t *page_table, const int32_t *seq_lens, void *out, int num_seqs,
+                    int n_q_heads, int n_kv_heads, float scale, int max_pages_per_seq,
+                    void *workspace, unsigned flags, bool self, hipStream_t stream)
+{
+    const int G = n_q_heads / n_kv_heads;
+    const WsLayout lay = ws_layout(num_seqs, G, n_kv_heads, max_pages_per_seq, forced_tiles(flags));
+    AttnArgs a = make_args(lay, workspace, num_seqs, n_q_heads, n_kv_heads, max_pages_per_seq,
+                           scale, flags);
+    a.q = (const uint16_t *)q;
+    a.k = (const uint16_t *)k_pages;
+    a.v = (const uint16_t *)v_pages;
+    a.pt = page_table;
+    a.seq_lens = seq_lens;
+    a.out = out;
+    return enqueue_attn(a, G, out_mode(flags), self, stream);
+}
 
 }  // namespace
 
@@ -1299,16 +1516,9 @@ int vd_decode_partial(const void *q, const void *k_pages, const void *v_pages,
         return st;
     if (num_seqs == 0)
         return VD_SUCCESS;
-    const int G = n_q_heads / n_kv_heads;
-    const WsLayout lay = ws_layout(num_seqs, G, n_kv_heads, max_pages_per_seq, forced_tiles(flags));
-    AttnArgs a = make_args(lay, workspace, n_q_heads, n_kv_heads, max_pages_per_seq, scale);
-    a.q = (const uint16_t *)q;
-    a.k = (const uint16_t *)k_pages;
-    a.v = (const uint16_t *)v_pages;
-    a.pt = page_table;
-    a.seq_lens = seq_lens;
-    a.out = out;
-    return enqueue_attn(a, G, out_mode(flags), stream);
+    return enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
+                           n_kv_heads, scale, max_pages_per_seq, workspace, flags,
+                           (flags & VD_FLAG_SELF_PLAN) != 0, stream);
 }
 
 int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, int head_dim,
@@ -1327,30 +1537,7 @@ int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, in
         return VD_ERROR_WORKSPACE_TOO_SMALL;
     if (num_seqs == 0)
         return VD_SUCCESS;
-    char *ws = (char *)workspace;
-    CombineArgs c;
-    c.out = out;
-    c.hdr = (const PlanHeader *)(ws + lay.hdr);
-    c.merge = (const int4 *)(ws + lay.merge);
-    c.part_ml = (const float2 *)(ws + lay.part_ml);
-    c.part_acc = (const float *)(ws + lay.part_acc);
-    c.Hq = n_q_heads;
-    c.Hkv = n_kv_heads;
-    c.G = G;
-    c.HW = heads_per_group(n_kv_heads);
-    c.list_len = num_seqs * (n_kv_heads / c.HW);
-    int cus = 0;
-    st = num_cus(&cus);
-    if (st)
-        return st;
-    // work items: at most one per (request, query head)
-    const long long items = std::max(1LL, (long long)num_seqs * n_q_heads);
-    const dim3 grid((unsigned)std::min<long long>((long long)cus * kCombineGroupsPerCU, items));
-    if (flags & VD_FLAG_OUT_F32)
-        hipLaunchKernelGGL(combine_kernel<MODE_F32>, grid, dim3(kCombineThreads), 0, stream, c);
-    else
-        hipLaunchKernelGGL(combine_kernel<MODE_BF16>, grid, dim3(kCombineThreads), 0, stream, c);
-    return launch_status();
+    return enqueue_combine(out, num_seqs, n_q_heads, n_kv_heads, lay, workspace, flags, stream);
 }
 
 int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
@@ -1366,17 +1553,14 @@ int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
         return st;
     if (num_seqs == 0)
         return VD_SUCCESS;
-    st = vd_decode_plan(seq_lens, num_seqs, n_q_heads, n_kv_heads, head_dim, page_size,
-                        max_pages_per_seq, workspace, workspace_bytes, flags, stream);
+    // self-planned attention, then the combine kernel
+    st = enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
+                         n_kv_heads, scale, max_pages_per_seq, workspace, flags, true, stream);
     if (st)
         return st;
-    st = vd_decode_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
-                           n_kv_heads, head_dim, page_size, scale, max_pages_per_seq, workspace,
-                           workspace_bytes, flags, stream);
-    if (st)
-        return st;
-    return vd_decode_combine(out, num_seqs, n_q_heads, n_kv_heads, head_dim, page_size,
-                             max_pages_per_seq, workspace, workspace_bytes, flags, stream);
+    const WsLayout lay = ws_layout(num_seqs, n_q_heads / n_kv_heads, n_kv_heads, max_pages_per_seq,
+                                   forced_tiles(flags));
+    return enqueue_combine(out, num_seqs, n_q_heads, n_kv_heads, lay, workspace, flags, stream);
 }
 
 int vd_decode_gather(const void *k_pages, const void *v_pages, const int32_t *page_table,
@@ -1403,14 +1587,15 @@ int vd_decode_gather(const void *k_pages, const void *v_pages, const int32_t *pa
                       MODE_GATHER, stream);
     if (st)
         return st;
-    AttnArgs a = make_args(lay, workspace, n_kv_heads, n_kv_heads, max_pages_per_seq, 1.0f);
+    AttnArgs a = make_args(lay, workspace, num_seqs, n_kv_heads, n_kv_heads, max_pages_per_seq,
+                           1.0f, 0);
     a.k = (const uint16_t *)k_pages;
     a.v = (const uint16_t *)v_pages;
     a.pt = page_table;
     a.seq_lens = seq_lens;
     a.out = k_out;
     a.out2 = v_out;
-    return enqueue_attn(a, 1, MODE_GATHER, stream);
+    return enqueue_attn(a, 1, MODE_GATHER, false, stream);
 }
 
 int vd_kv_append(const void *k_new, const void *v_new, void *k_pages, void *v_pages,

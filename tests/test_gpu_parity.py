@@ -258,7 +258,9 @@ def test_gqa_ratios(G, hkv):
 
 def test_max_requests():
     """8192 requests (the supported maximum): every planner thread owns eight
-    requests; mixed tiny, empty and one long request."""
+    requests, every thread of a self-planning attention workgroup 64; mixed
+    tiny, empty and one long request.  Staged and whole step agree bit for
+    bit."""
     rng = np.random.default_rng(40)
     lengths = [int(x) for x in rng.choice([0, 1, 2, 7, 16, 17, 40], 8192)]
     lengths[4097] = 5000
@@ -266,7 +268,17 @@ def test_max_requests():
     c = custom(lengths, hq=8, hkv=2, seed=41)
     d = dev_case(c)
     ref = ref_of(c)
-    check_f32(run_gpu(d), ref, "8192 requests")
+    whole = run_gpu(d)
+    check_f32(whole, ref, "8192 requests")
+    maxp = c["max_pages_per_seq"]
+    ws = vd.alloc_workspace(8192, 8, 2, maxp)
+    staged = torch.full(d["q"].shape, float("nan"), dtype=torch.float32, device=DEV)
+    vd.vd_decode_plan(d["seq_lens"], 8, 2, maxp, ws)
+    vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
+                         staged, d["scale"], ws)
+    vd.vd_decode_combine(staged, 2, maxp, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(whole.view(torch.int32).cpu(), staged.view(torch.int32).cpu())
 
 
 @pytest.mark.parametrize("G,hkv", [(16, 1), (16, 2), (8, 2)])
@@ -335,8 +347,62 @@ def test_staged_plan_once_two_layers():
     assert torch.equal(outs[0].view(torch.int32).cpu(), fused.view(torch.int32).cpu())
 
 
+@pytest.mark.parametrize("case", ["tiny_b4", "long_b16", "mixed", "mixed_forced7", "split_many"])
+def test_staged_equals_whole_step(case):
+    """The whole step plans inside the attention kernel; the staged API runs
+    the planner kernel first.  Both cut the same ranges, so their outputs
+    agree bit for bit, in both output types."""
+    say("case: staged vs whole step, %s" % case)
+    flags = 0
+    if case in ("tiny_b4", "long_b16"):
+        c = make_case(case, seed=0, fill="nan")
+    elif case == "split_many":
+        c = custom([16384, 3, 0, 9000], seed=21)
+    else:
+        c = custom([0, 5, 300, 0, 2049, 1, 16, 17, 7000, 0], seed=22)
+        flags = vd.VD_FLAG_RANGE_TILES(7) if case == "mixed_forced7" else 0
+    d = dev_case(c)
+    B, Hq, Hkv, maxp = c["num_seqs"], c["n_q_heads"], c["n_kv_heads"], c["max_pages_per_seq"]
+    for dt in (torch.float32, torch.bfloat16):
+        whole = run_gpu(d, dt, flags=flags)
+        ws = vd.alloc_workspace(B, Hq, Hkv, maxp, flags)
+        staged = torch.full(d["q"].shape, float("nan"), dtype=dt, device=DEV)
+        vd.vd_decode_plan(d["seq_lens"], Hq, Hkv, maxp, ws, flags=flags)
+        vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
+                             staged, d["scale"], ws, flags=flags)
+        vd.vd_decode_combine(staged, Hkv, maxp, ws, flags=flags)
+        # the self-planned kernel through the staged calls, on a workspace
+        # that still holds the planner's tables
+        selfp = torch.full(d["q"].shape, float("nan"), dtype=dt, device=DEV)
+        vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
+                             selfp, d["scale"], ws, flags=flags | vd.VD_FLAG_SELF_PLAN)
+        vd.vd_decode_combine(selfp, Hkv, maxp, ws, flags=flags)
+        torch.cuda.synchronize()
+        iv = torch.int32 if dt == torch.float32 else torch.int16
+        assert torch.equal(whole.view(iv).cpu(), staged.view(iv).cpu()), case
+        assert torch.equal(whole.view(iv).cpu(), selfp.view(iv).cpu()), case
+    check_f32(run_gpu(d, flags=flags), ref_of(c), case)
+
+
+def test_workspace_reuse_across_steps():
+    """One workspace serves steps of different length mixes in a row: what a
+    longer step left in it (ranges, boundary records, partials) never leaks
+    into a later, smaller one."""
+    say("case: workspace reuse across steps")
+    mixes = [[9000, 4000, 2500, 777], [0, 33, 0, 5], [0, 0, 0, 0], [16, 16, 16, 16], [12000, 1, 0, 40]]
+    maxp = (12000 + 15) // 16
+    ws = vd.alloc_workspace(4, 32, 8, maxp)
+    for i, lens in enumerate(mixes):
+        c = custom(lens, seed=40 + i, pt_stride=maxp)
+        d = dev_case(c)
+        got = run_gpu(d, ws=ws)
+        fresh = run_gpu(d)
+        assert torch.equal(got.view(torch.int32).cpu(), fresh.view(torch.int32).cpu()), lens
+        check_f32(got, ref_of(c), "reuse step %d" % i)
+
+
 def test_hip_graph_replay():
-    """A whole step (plan, attention, combine kernels) captured into a HIP
+    """A whole step (attention and combine kernels) captured into a HIP
     graph: every replay, with eager work and a synchronisation between
     replays, equals the eager result bit for bit, and a replay after new Q
     values are written in place gives the new eager result."""
