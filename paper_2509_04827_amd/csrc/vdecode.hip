@@ -475,9 +475,11 @@ __device__ inline PageIds load_page_ids(const int32_t *pt_row, int jb, int je, i
     return p;
 }
 
-// Plan tables and request lengths are not written while the attention kernel
-// runs: read them through the constant address space, which gives scalar
-// loads that are counted apart from the K/V stream.
+// The planner's tables and the request lengths are not written while the
+// attention kernel runs (a self-planned kernel writes only the header,
+// boundary records and empty-request list, which it never reads): read them
+// through the constant address space, which gives scalar loads that are
+// counted apart from the K/V stream.
 typedef const __attribute__((address_space(4))) int32_t *const_i32p;
 
 // A piece: pages [jb, je) of KV-head group q of request b, cut from range w.
