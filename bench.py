@@ -1,11 +1,13 @@
 """Decode-attention benchmark on one MI355X.
 
 One step = one whole decode-attention call (self-planned attention kernel +
-combine kernel) over
-the chat-like batch: 256 requests, 32 query / 8 KV heads, head_dim 128,
+combine kernel) over the chat-like batch: 256 requests, 32 query / 8 KV heads, head_dim 128,
 lengths lognormal (median 1200, sigma 0.8) clipped to [16, 16384], 16-token
 pages in shuffled order, bf16 N(0,1) values, seed 0 (synthetic; stands in for
 chat-trace length mixes).  Inputs are resident in HBM before timing starts.
+Before the warm-up steps, steps run untimed for --settle seconds: an idle
+MI355X drops its shader clock to about 100 MHz and takes milliseconds of
+work to return to 2.4 GHz.
 
 Prints one JSON line:
   value         KV bytes per step / step time, GB/s (whole job, all N GPUs)
@@ -66,6 +68,21 @@ def committed_traffic(workload: str):
     return t.get("hbm_bytes_per_launch")
 
 
+def settle_clocks(fn, seconds: float) -> int:
+    """Run fn (one step) for `seconds` of wall time before anything is timed.
+    Between jobs the GPU sits in a deep-sleep clock state (about 100 MHz
+    against its 2.4 GHz) and needs milliseconds of steady work to come back,
+    so a few tens of warm-up steps end too early.  Returns the steps run."""
+    import torch
+    n, t0 = 0, time.time()
+    while time.time() - t0 < seconds:
+        for _ in range(16):
+            fn()
+        torch.cuda.synchronize()
+        n += 16
+    return n
+
+
 SURFACE_BATCH = (1, 2, 4, 8, 16, 32, 64, 128, 256, 512)
 SURFACE_LEN = (16, 64, 256, 1024, 4096, 16384)
 SURFACE_GQA8_BATCH = (64, 128, 256)
@@ -114,16 +131,10 @@ def latency_surface(outdir: str, iters: int = 10, warmup: int = 3):
         ws = vd.alloc_workspace(B, Hq, Hkv, maxp)
         scale = float(np.float32(1.0 / np.sqrt(D)))
 
-        def step(e0=None, e1=None):
-            if e0 is None:
-                vd.vd_decode_attn(q, kp, vp, ptd, sl, out, scale, ws, stream=stream)
-                return
-            e0.record(stream)
-            vd.vd_decode_partial(q, kp, vp, ptd, sl, out, scale, ws, flags=vd.VD_FLAG_SELF_PLAN,
-                                 stream=stream)
-            e1.record(stream)
-            vd.vd_decode_combine(out, Hkv, maxp, ws, stream=stream)
+        def step():
+            vd.vd_decode_attn(q, kp, vp, ptd, sl, out, scale, ws, stream=stream)
 
+        settle_clocks(step, 0.02)
         for _ in range(warmup):
             step()
         st, en = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -134,13 +145,15 @@ def latency_surface(outdir: str, iters: int = 10, warmup: int = 3):
         en.record(stream)
         torch.cuda.synchronize()
         us_step = st.elapsed_time(en) * 1e3 / iters
-        # attention alone: events around it, in separate steps (see main())
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(iters)]
-        for e0, e1 in ev:
-            step(e0, e1)
+        # the attention kernel alone: the same launches back to back (see main())
+        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ea.record(stream)
+        for _ in range(iters):
+            vd.vd_decode_partial(q, kp, vp, ptd, sl, out, scale, ws, flags=vd.VD_FLAG_SELF_PLAN,
+                                 stream=stream)
+        eb.record(stream)
         torch.cuda.synchronize()
-        us_attn = float(np.median([a.elapsed_time(b) for a, b in ev])) * 1e3
+        us_attn = ea.elapsed_time(eb) * 1e3 / iters
         # the same step captured into a HIP graph and replayed: no host launch
         # cost per kernel, so small steps show the device-side floor
         side = torch.cuda.Stream()
@@ -233,6 +246,7 @@ def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
     rows = []
 
     def timed(fn):
+        settle_clocks(fn, 0.02)
         for _ in range(warmup):
             fn()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -278,8 +292,11 @@ def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--settle", type=float, default=0.3, metavar="SECONDS",
+                    help="untimed steps for this long before the warm-up steps, so that the "
+                         "GPU has left its idle clock state")
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the flushed-cache step timings")
@@ -350,6 +367,7 @@ def main():
         ev1.record(stream)
         vd.vd_decode_combine(out, Hkv, maxp, ws, stream=stream)
 
+    settle_steps = settle_clocks(step, args.settle)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -367,18 +385,25 @@ def main():
     ms_total = start.elapsed_time(stop)
     ms_step = ms_total / K
 
-    # The attention kernel's average launch duration: the same K steps again
-    # with events around each attention launch.  An event between kernels
-    # costs the step a few microseconds, so these stay out of the region
-    # above.
-    a0 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
-    a1 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    # The attention kernel's average launch duration: K launches of the
+    # step's attention kernel (vd_decode_partial with VD_FLAG_SELF_PLAN, the
+    # kernel vd_decode_attn runs) back to back, events around the K.  Events
+    # around each launch would also count its dispatch and end-of-kernel
+    # write-back, a few microseconds each.
+    def attn_only():
+        vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws, flags=vd.VD_FLAG_SELF_PLAN,
+                             stream=stream)
+
+    for _ in range(args.warmup):
+        attn_only()
+    a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    for i in range(K):
-        step(a0[i], a1[i])
+    a0.record(stream)
+    for _ in range(K):
+        attn_only()
+    a1.record(stream)
     torch.cuda.synchronize()
-    attn_ms = [a0[i].elapsed_time(a1[i]) for i in range(K)]
-    attn_avg_ms = float(np.mean(attn_ms))
+    attn_avg_ms = a0.elapsed_time(a1) / K
 
     # Cold caches: a 1 GiB write (beyond the 256 MB Infinity Cache and the
     # L2s) before each step; per-step events, outside the back-to-back timing.
@@ -471,6 +496,7 @@ def main():
         "n_gpus": 1,
         "steps": K,
         "warmup": args.warmup,
+        "settle": {"seconds": args.settle, "steps": settle_steps},
         "ms_per_step": round(ms_step, 5),
         "us_per_step": round(ms_step * 1e3, 2),
         "pct_of_peak": round(100.0 * value / PEAK_HBM_GBS, 2),
