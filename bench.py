@@ -229,6 +229,120 @@ GEMM_M = (1, 2, 4, 8, 16, 24, 32, 48, 64, 96, 128, 160, 192, 224, 240, 248, 255,
           272, 288, 320, 384, 448, 512, 513, 640, 768, 1024)
 
 
+def step_record(raw) -> dict:
+    """Decode a workspace's step record (vd_step_info, the first 48 bytes;
+    raw: uint8 numpy array): sizes, the first attention workgroup's time in
+    us and the mean shader clock over it in MHz (real-time counter at
+    100 MHz)."""
+    import numpy as np
+    raw = np.ascontiguousarray(raw[:48])
+    n = raw[:16].view(np.int32)
+    t0, c0, t1, c1 = (int(x) for x in raw[16:48].view(np.uint64))
+    dt = max(t1 - t0, 1)
+    return {"n_ranges": int(n[0]), "n_tiles": int(n[1]), "n_empty": int(n[2]),
+            "first_group_us": dt * 0.01, "sclk_mhz": (c1 - c0) * 100.0 / dt}
+
+
+def clock_sweep(outdir: str, bursts: int = 10, steps: int = 60, idle_s: float = 1.5):
+    """Attention-kernel time against the shader clock it ran at: the
+    frequency-latency relation T ~ f^-beta of Sec. 3.2 (Eq. t-alpha-beta)
+    for decode attention on MI355X.  Clocks cannot be set from user space.
+    Instead each burst of whole chat_b256 steps starts after the GPU has
+    idled, and the power manager moves the shader clock over the burst's
+    first tens of steps (between about 1.4 and 2.4 GHz; the memory clock
+    stays fixed).  Each step's record (vd_step_info: the shader clock over
+    the attention kernel's first workgroup) is copied aside on the stream,
+    and events bracket each attention launch.  A burst's first step is left
+    out.  Fits ln T = a - beta ln f by least squares, for the event time and
+    for the first workgroup's time."""
+    import numpy as np
+    import torch
+
+    import paper_2509_04827_amd as vd
+    from workloads import make_case
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    c = make_case(WORKLOAD, seed=0, fill="zero")
+    q, k, v = c["q"].to(dev), c["k_pages"].to(dev), c["v_pages"].to(dev)
+    pt, sl = c["page_table"].to(dev), c["seq_lens"].to(dev)
+    out = torch.empty(q.shape, dtype=torch.bfloat16, device=dev)
+    B, Hq, Hkv, maxp = c["num_seqs"], c["n_q_heads"], c["n_kv_heads"], c["max_pages_per_seq"]
+    ws = vd.alloc_workspace(B, Hq, Hkv, maxp)
+    stream = torch.cuda.current_stream()
+    hist = torch.empty((steps, 48), dtype=torch.uint8, device=dev)
+    rows = []
+    for burst in range(bursts):
+        torch.cuda.synchronize()
+        time.sleep(idle_s)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+        for i, (e0, e1) in enumerate(ev):
+            e0.record(stream)
+            vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws,
+                                 flags=vd.VD_FLAG_SELF_PLAN, stream=stream)
+            e1.record(stream)
+            vd.vd_decode_combine(out, Hkv, maxp, ws, stream=stream)
+            hist[i].copy_(ws[:48])
+        torch.cuda.synchronize()
+        h = hist.cpu().numpy()
+        for i, (e0, e1) in enumerate(ev):
+            if i == 0:   # its events also span the GPU's wake-up from idle (up to ms)
+                continue
+            r = step_record(h[i])
+            rows.append({"burst": burst, "step": i, "us_attn": round(e0.elapsed_time(e1) * 1e3, 2),
+                         "us_first_group": round(r["first_group_us"], 2),
+                         "sclk_mhz": round(r["sclk_mhz"], 1)})
+        print("clock sweep: burst %d, shader clock %.0f-%.0f MHz" % (
+            burst, min(x["sclk_mhz"] for x in rows[1 - steps:]), max(x["sclk_mhz"] for x in rows[1 - steps:])),
+            file=sys.stderr, flush=True)
+    f = np.array([r["sclk_mhz"] for r in rows])
+
+    def fit(col):
+        T = np.array([r[col] for r in rows])
+        A = np.vstack([np.ones_like(f), np.log(f)]).T
+        (a, b), *_ = np.linalg.lstsq(A, np.log(T), rcond=None)
+        resid = np.log(T) - A @ np.array([a, b])
+        r2 = 1.0 - resid.var() / np.log(T).var()
+        return {"beta": round(float(-b), 4), "r2": round(float(r2), 3),
+                "us_at_2400": round(float(np.exp(a + b * np.log(2400.0))), 2)}
+
+    bins = []
+    edges = [1300, 1500, 1700, 1900, 2100, 2300, 2500]
+    for lo, hi in zip(edges, edges[1:]):
+        sel = [r for r in rows if lo <= r["sclk_mhz"] < hi]
+        if sel:
+            bins.append({"sclk_lo": lo, "sclk_hi": hi, "n": len(sel),
+                         "sclk_median": round(float(np.median([r["sclk_mhz"] for r in sel])), 1),
+                         "us_attn_median": round(float(np.median([r["us_attn"] for r in sel])), 2),
+                         "us_first_group_median": round(float(np.median([r["us_first_group"] for r in sel])), 2)})
+
+    def fit_bins(col):
+        # per-bin medians, weighted by the points in each bin: robust to the
+        # odd event interval that also holds a host-side delay
+        fb = np.array([b["sclk_median"] for b in bins])
+        Tb = np.array([b[col] for b in bins])
+        wb = np.sqrt(np.array([b["n"] for b in bins], dtype=float))
+        A = np.vstack([np.ones_like(fb), np.log(fb)]).T * wb[:, None]
+        (a, b), *_ = np.linalg.lstsq(A, np.log(Tb) * wb, rcond=None)
+        return round(float(-b), 4)
+
+    res = {"points": len(rows), "sclk_mhz_min": round(float(f.min()), 1),
+           "sclk_mhz_max": round(float(f.max()), 1),
+           "first_group": fit("us_first_group"), "attn_events": fit("us_attn"),
+           "beta_first_group_bins": fit_bins("us_first_group_median"),
+           "beta_attn_events_bins": fit_bins("us_attn_median"), "bins": bins}
+    os.makedirs(outdir, exist_ok=True)
+    with open(os.path.join(outdir, "decode_clock_sweep.csv"), "w") as fh:
+        fh.write("burst,step,us_attn,us_first_group,sclk_mhz\n")
+        for r in rows:
+            fh.write("%d,%d,%.2f,%.2f,%.1f\n" % (r["burst"], r["step"], r["us_attn"],
+                                                  r["us_first_group"], r["sclk_mhz"]))
+    with open(os.path.join(outdir, "decode_clock_sweep.json"), "w") as fh:
+        json.dump(res, fh, indent=1)
+    print(json.dumps(res), flush=True)
+
+
 def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
     """Decode-step projection GEMMs of a Llama-3-8B-shaped layer (hidden 4096,
     KV 8 x 128, MLP 14336) over the decode batch M: this library's
@@ -309,6 +423,9 @@ def main():
     ap.add_argument("--gemm-sweep", metavar="DIR", default=None,
                     help="instead of the bench line, time the decode-step projection GEMMs "
                          "over the batch size and write DIR/decode_gemm_sweep.csv")
+    ap.add_argument("--clock-sweep", metavar="DIR", default=None,
+                    help="instead of the bench line, time the attention kernel against the "
+                         "shader clock it ran at and write DIR/decode_clock_sweep.{csv,json}")
     ap.add_argument("--surface", metavar="DIR", default=None,
                     help="instead of the bench line, measure the latency surface over "
                          "(batch, tokens per request) and write DIR/decode_latency_surface.{csv,md}")
@@ -332,6 +449,9 @@ def main():
         return
     if args.gemm_sweep:
         gemm_sweep(args.gemm_sweep)
+        return
+    if args.clock_sweep:
+        clock_sweep(args.clock_sweep)
         return
 
     w = WORKLOADS[args.workload]
@@ -384,6 +504,8 @@ def main():
     torch.cuda.synchronize()
     ms_total = start.elapsed_time(stop)
     ms_step = ms_total / K
+    # the last timed step's record: the shader clock its attention kernel ran at
+    rec = step_record(ws[:48].cpu().numpy())
 
     # The attention kernel's average launch duration: K launches of the
     # step's attention kernel (vd_decode_partial with VD_FLAG_SELF_PLAN, the
@@ -516,6 +638,7 @@ def main():
                      "frac_of_stream_ceiling": round(achieved / ceiling, 4) if ceiling else None},
         "cold_cache": cold,
         "cpu_baseline": cpu,
+        "sclk_mhz": round(rec["sclk_mhz"], 1),
     }
     print(json.dumps(line), flush=True)
 

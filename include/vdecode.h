@@ -86,6 +86,28 @@ typedef enum vd_status {
 const char *vd_status_string(int status);
 
 /*
+ * Step record.  Every attention launch (vd_decode_attn, vd_decode_partial,
+ * vd_decode_gather) leaves one at offset 0 of its workspace, written by the
+ * kernel's first workgroup when it finishes: the plan's sizes, and two
+ * device counters read when that workgroup starts and ends.  The counters
+ * give the shader clock the step ran at, the quantity the paper's
+ * frequency-latency relation is stated in (Sec. 3.2, Eq. t-alpha-beta):
+ *   t_start, t_end      the constant-rate real-time counter (100 MHz on
+ *                       MI355X)
+ *   clk_start, clk_end  the shader-clock cycle counter
+ * Mean shader clock in MHz = (clk_end - clk_start) * 100 / (t_end - t_start).
+ * Read it after the call has completed (e.g. hipMemcpyAsync on the same
+ * stream); the next call on the workspace overwrites it.
+ */
+typedef struct vd_step_info {
+    int32_t n_ranges;    /* ranges the step's tiles were cut into */
+    int32_t n_tiles;     /* (page, KV-head group) tiles */
+    int32_t n_empty;     /* requests without tokens */
+    int32_t reserved;
+    uint64_t t_start, clk_start, t_end, clk_end;
+} vd_step_info;
+
+/*
  * Bytes of device workspace a call with these sizes needs: the plan and the
  * split-K partials (per partial and query head: running max, normaliser and
  * an fp32 head_dim accumulator).  Independent of the actual lengths; grows

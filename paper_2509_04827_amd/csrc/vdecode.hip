@@ -97,12 +97,10 @@ typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
-struct PlanHeader {
-    int n_ranges;  // W
-    int n_tiles;   // T
-    int n_empty;   // requests without tokens (listed for the combine kernel)
-    int pad[5];
-};
+// The workspace header is the step record of the C ABI (vd_step_info):
+// planner or self-planned prologue fill its sizes, the attention kernel's
+// first workgroup its clock stamps.
+typedef vd_step_info PlanHeader;
 
 // ---------------------------------------------------------------- workspace
 struct WsLayout {
@@ -828,8 +826,7 @@ __device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageI
 // piece's last page is consumed, so the K/V stream of a wave runs on across
 // piece boundaries.
 template <int G, int MODE, bool SELF>
-__global__ void __launch_bounds__(kAttnMaxThreads)
-attn_kernel(const AttnArgs a)
+__device__ inline void attn_body(const AttnArgs &a)
 {
     const int lane = threadIdx.x & 63;
     const int hi = threadIdx.x >> 6;          // KV head within the group
@@ -965,6 +962,24 @@ attn_kernel(const AttnArgs a)
             qreg[3] = nq[3];
         }
         flush();
+    }
+}
+
+// The first workgroup stamps the step record with the real-time and
+// shader-clock counters at its start and end.
+template <int G, int MODE, bool SELF>
+__global__ void __launch_bounds__(kAttnMaxThreads)
+attn_kernel(const AttnArgs a)
+{
+    const bool stamp = blockIdx.x == 0 && threadIdx.x == 0;
+    if (stamp) {
+        a.hdr->t_start = __builtin_amdgcn_s_memrealtime();
+        a.hdr->clk_start = __builtin_amdgcn_s_memtime();
+    }
+    attn_body<G, MODE, SELF>(a);
+    if (stamp) {
+        a.hdr->t_end = __builtin_amdgcn_s_memrealtime();
+        a.hdr->clk_end = __builtin_amdgcn_s_memtime();
     }
 }
 

@@ -384,6 +384,52 @@ def test_staged_equals_whole_step(case):
     check_f32(run_gpu(d, flags=flags), ref_of(c), case)
 
 
+def _step_record(ws):
+    raw = ws[:48].cpu().numpy()
+    n = raw[:16].view(np.int32)
+    t0, c0, t1, c1 = (int(x) for x in raw[16:48].view(np.uint64))
+    return n, t0, c0, t1, c1
+
+
+def test_step_record():
+    """The step record at the head of the workspace (vd_step_info): the
+    plan's tile and empty-request counts, and real-time / shader-clock
+    stamps of the first workgroup that fit inside the launch and give a
+    plausible clock."""
+    say("case: step record")
+    lens = [37, 700, 4100, 0, 260]
+    c = custom(lens, seed=23)
+    d = dev_case(c)
+    tiles = sum((x + 15) // 16 for x in lens) * 2          # 8 KV heads in groups of 4
+    for staged in (False, True):
+        ws = vd.alloc_workspace(5, 32, 8, c["max_pages_per_seq"])
+        ws.zero_()
+        out = torch.empty(d["q"].shape, dtype=torch.float32, device=DEV)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        flags = 0
+        if staged:
+            vd.vd_decode_plan(d["seq_lens"], 32, 8, c["max_pages_per_seq"], ws)
+        else:
+            flags = vd.VD_FLAG_SELF_PLAN
+        e0.record()
+        vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
+                             out, d["scale"], ws, flags=flags)
+        e1.record()
+        vd.vd_decode_combine(out, 8, c["max_pages_per_seq"], ws)
+        torch.cuda.synchronize()
+        n, t0, c0, t1, c1 = _step_record(ws)
+        us_event = e0.elapsed_time(e1) * 1e3
+        us_first = (t1 - t0) * 0.01
+        mhz = (c1 - c0) * 100.0 / max(t1 - t0, 1)
+        say("  staged %s: ranges %d tiles %d empty %d, first group %.1f us (launch %.1f us), "
+            "shader clock %.0f MHz" % (staged, n[0], n[1], n[2], us_first, us_event, mhz))
+        assert n[1] == tiles and n[2] == 1 and 1 <= n[0] <= tiles
+        assert t1 > t0 and c1 > c0
+        assert us_first <= 1.5 * us_event + 20.0
+        assert 50.0 <= mhz <= 3500.0
+        check_f32(out, ref_of(c), "step record run")
+
+
 def test_workspace_reuse_across_steps():
     """One workspace serves steps of different length mixes in a row: what a
     longer step left in it (ranges, boundary records, partials) never leaks
