@@ -231,11 +231,12 @@ int vd_gemm_bf16(const void *x, const void *w, void *y, int M, int N, int K,
 
 /*
  * Measurement aid, not part of the attention path: reads `bytes` (a multiple
- * of 16) from device buffer `buf` with 16-byte non-temporal loads from
- * `blocks` workgroups of 256 threads, and may write 4 bytes to device pointer
- * `sink` (so the reads cannot be optimised away).  Timing it gives the HBM
- * read rate this device sustains, the practical ceiling for vd_decode_attn.
- * buf 16-byte aligned, sink 4-byte aligned, blocks > 0.
+ * of 16) from device buffer `buf` with 16-byte non-temporal loads, each of at
+ * most `blocks` workgroups of 256 threads streaming one contiguous chunk,
+ * and may write 4 bytes to device pointer `sink` (so the reads cannot be
+ * optimised away).  Timing it gives the HBM read rate this device sustains,
+ * the practical ceiling for vd_decode_attn.  buf 16-byte aligned, sink
+ * 4-byte aligned, blocks > 0.
  */
 int vd_stream_read(const void *buf, size_t bytes, void *sink, int blocks,
                    hipStream_t stream);

@@ -190,7 +190,7 @@ def vd_gemm_bf16(x, w, y, workspace=None, flags: int = 0, stream=None) -> None:
                               _out_flags(y, flags), _stream(stream)), "vd_gemm_bf16")
 
 
-def vd_stream_read(buf, sink, blocks: int = 8192, stream=None) -> None:
+def vd_stream_read(buf, sink, blocks: int = 16384, stream=None) -> None:
     """Read all of `buf` (a measurement of the HBM read rate; see the header)."""
     _check(lib().vd_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), int(blocks),
                                 _stream(stream)), "vd_stream_read")
