@@ -235,6 +235,37 @@ def test_pt_stride():
     check_f32(run_gpu(dev_case(c)), ref_of(c), "pt stride 200")
 
 
+def test_length_clamped_to_table():
+    """A length past the page table's capacity (max_pages_per_seq * 16) is
+    clamped to it: the result equals that of the capacity itself, bit for
+    bit, in the whole step, the staged calls and the gather."""
+    say("case: lengths clamped to the table")
+    c = custom([40, 160, 7], seed=24, pt_stride=10)       # 10 pages = 160 tokens
+    d = dev_case(c)
+    ref = run_gpu(d)
+    check_f32(ref, ref_of(c), "at capacity")
+    d2 = dict(d)
+    d2["seq_lens"] = torch.tensor([40, 1000, 7], dtype=torch.int32, device=DEV)
+    assert torch.equal(run_gpu(d2).view(torch.int32).cpu(), ref.view(torch.int32).cpu())
+    ws = vd.alloc_workspace(3, 32, 8, 10)
+    staged = torch.empty_like(ref)
+    vd.vd_decode_plan(d2["seq_lens"], 32, 8, 10, ws)
+    vd.vd_decode_partial(d2["q"], d2["k_pages"], d2["v_pages"], d2["page_table"], d2["seq_lens"],
+                         staged, d2["scale"], ws)
+    vd.vd_decode_combine(staged, 8, 10, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(staged.view(torch.int32).cpu(), ref.view(torch.int32).cpu())
+    n = 40 + 160 + 7
+    ko = torch.empty((n, 8, 128), dtype=torch.bfloat16, device=DEV)
+    vo = torch.empty_like(ko)
+    gws = vd.alloc_workspace(3, 8, 8, 10)
+    vd.vd_decode_gather(d2["k_pages"], d2["v_pages"], d2["page_table"], d2["seq_lens"], ko, vo, gws)
+    torch.cuda.synchronize()
+    kr, vr = oracle.gather(bits(c["k_pages"]), bits(c["v_pages"]), c["page_table"].numpy(),
+                           c["seq_lens"].numpy())
+    assert np.array_equal(bits(ko.cpu()), kr) and np.array_equal(bits(vo.cpu()), vr)
+
+
 # ------------------------------------------------------------------ shapes and edges
 def test_page_boundary_lengths():
     lengths = [1, 15, 16, 17, 31, 32, 33, 255, 256, 257, 1023, 1024, 1025]
