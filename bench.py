@@ -416,7 +416,8 @@ def main():
     ap.add_argument("--no-cold", action="store_true", help="skip the flushed-cache step timings")
     ap.add_argument("--no-ceiling", action="store_true", help="skip the HBM read-ceiling run")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="stop repeating the oracle after this much wall time")
+                    help="repeat the oracle over the whole step for this much wall time "
+                         "(at least 3 runs)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="after timing, copy a BYTES-sized buffer 3 times (a plain copy "
                          "kernel of known size, to scale HBM counters by)")
@@ -597,7 +598,7 @@ def main():
             t1 = time.time()
             oracle.decode_attn(hq, hk, hv, hpt, hsl, c["scale"])
             times.append(time.time() - t1)
-            if time.time() >= t_end or len(times) >= 5:
+            if (time.time() >= t_end and len(times) >= 3) or len(times) >= 200:
                 break
         sec = float(np.median(times))
         cpu_model = None
