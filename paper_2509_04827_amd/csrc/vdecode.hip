@@ -74,9 +74,9 @@ namespace {
 
 constexpr int kHeadDim = 128;
 constexpr int kPage = 16;
-constexpr int kMaxSeqs = 8192;         // planner keeps tile offsets in LDS
+constexpr int kMaxSeqs = 8192;         // every request's tile offset fits in LDS when planning
 constexpr int kMaxRangeTiles = 512;    // eight 64-entry page-id windows per piece
-constexpr int kMinRangeTiles = 4;      // small steps: at least this many tiles per range
+constexpr int kMinRangeTiles = 4;      // small steps: ranges of at least min(this, mean segment) tiles
 constexpr int kMaxResidentGroups = 4096;
 constexpr int kPlanThreads = 1024;
 constexpr int kHeadsPerGroup = 4;      // preferred KV heads (waves) per attention workgroup
@@ -821,10 +821,10 @@ __device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageI
 }
 
 // Each workgroup walks its ranges piece by piece, HW waves per piece (one KV
-// head each).  The next piece's descriptor (scalar loads), page ids and Q
-// operand are loaded at the start of a piece, and its first page while the
-// piece's last page is consumed, so the K/V stream of a wave runs on across
-// piece boundaries.
+// head each).  The next piece's bounds (a scalar load of its request's
+// length), page ids and Q operand are fetched at the start of a piece, and
+// its first page while the piece's last page is consumed, so the K/V stream
+// of a wave runs on across piece boundaries.
 template <int G, int MODE, bool SELF>
 __device__ inline void attn_body(const AttnArgs &a)
 {
