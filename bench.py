@@ -229,20 +229,6 @@ GEMM_M = (1, 2, 4, 8, 16, 24, 32, 48, 64, 96, 128, 160, 192, 224, 240, 248, 255,
           272, 288, 320, 384, 448, 512, 513, 640, 768, 1024)
 
 
-def step_record(raw) -> dict:
-    """Decode a workspace's step record (vd_step_info, the first 48 bytes;
-    raw: uint8 numpy array): sizes, the first attention workgroup's time in
-    us and the mean shader clock over it in MHz (real-time counter at
-    100 MHz)."""
-    import numpy as np
-    raw = np.ascontiguousarray(raw[:48])
-    n = raw[:16].view(np.int32)
-    t0, c0, t1, c1 = (int(x) for x in raw[16:48].view(np.uint64))
-    dt = max(t1 - t0, 1)
-    return {"n_ranges": int(n[0]), "n_tiles": int(n[1]), "n_empty": int(n[2]),
-            "first_group_us": dt * 0.01, "sclk_mhz": (c1 - c0) * 100.0 / dt}
-
-
 def clock_sweep(outdir: str, bursts: int = 10, steps: int = 60, idle_s: float = 1.5):
     """Attention-kernel time against the shader clock it ran at: the
     frequency-latency relation T ~ f^-beta of Sec. 3.2 (Eq. t-alpha-beta)
@@ -285,11 +271,11 @@ def clock_sweep(outdir: str, bursts: int = 10, steps: int = 60, idle_s: float = 
             vd.vd_decode_combine(out, Hkv, maxp, ws, stream=stream)
             hist[i].copy_(ws[:48])
         torch.cuda.synchronize()
-        h = hist.cpu().numpy()
+        h = hist.cpu()
         for i, (e0, e1) in enumerate(ev):
             if i == 0:   # its events also span the GPU's wake-up from idle (up to ms)
                 continue
-            r = step_record(h[i])
+            r = vd.step_info(h[i])
             rows.append({"burst": burst, "step": i, "us_attn": round(e0.elapsed_time(e1) * 1e3, 2),
                          "us_first_group": round(r["first_group_us"], 2),
                          "sclk_mhz": round(r["sclk_mhz"], 1)})
@@ -506,7 +492,7 @@ def main():
     ms_total = start.elapsed_time(stop)
     ms_step = ms_total / K
     # the last timed step's record: the shader clock its attention kernel ran at
-    rec = step_record(ws[:48].cpu().numpy())
+    rec = vd.step_info(ws)
 
     # The attention kernel's average launch duration: K launches of the
     # step's attention kernel (vd_decode_partial with VD_FLAG_SELF_PLAN, the

@@ -6,8 +6,10 @@ HIP kernels of ``libvdecode.so``, reached through its C ABI
 streams.  There is no fallback: if the library is not built, every call
 raises.
 
-The functions carry the C names; tensors stand in for pointers and the sizes
-are read from their shapes:
+The functions carry the C names; tensors stand in for pointers (contiguous,
+on the device; dtypes checked) and the sizes are read from their shapes.
+step_info(workspace) reads back the step record (vd_step_info) an attention
+call leaves at the head of its workspace.
 
     q          bf16  [num_seqs, n_q_heads, head_dim]           (cuda)
     k_pages    bf16  [num_pages, page_size, n_kv_heads, head_dim]
@@ -103,7 +105,40 @@ def alloc_workspace(num_seqs, n_q_heads, n_kv_heads, max_pages_per_seq, flags=0,
 
 
 def _ptr(t):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+    """Device address of a tensor the kernels read or write as a dense array."""
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("libvdecode needs contiguous tensors (got strides %s)" % (t.stride(),))
+    if t.device.type != "cuda":
+        raise ValueError("libvdecode needs device tensors (got one on %s)" % t.device)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype(t, allowed, what):
+    if t.dtype not in allowed:
+        raise ValueError("%s must be %s (got %s)" % (what, " or ".join(map(str, allowed)), t.dtype))
+
+
+def _attn_dtypes(q, k_pages, v_pages, page_table, seq_lens, out):
+    for t, n in ((q, "q"), (k_pages, "k_pages"), (v_pages, "v_pages")):
+        _dtype(t, (torch.bfloat16,), n)
+    _dtype(page_table, (torch.int32,), "page_table")
+    _dtype(seq_lens, (torch.int32,), "seq_lens")
+    _dtype(out, (torch.bfloat16, torch.float32), "out")
+
+
+def step_info(workspace) -> dict:
+    """The step record (vd_step_info) an attention call left at the head of
+    `workspace`, read back to the host (synchronises with the device): the
+    plan's sizes, the first workgroup's time in microseconds and the mean
+    shader clock over it in MHz (real-time counter at 100 MHz)."""
+    raw = workspace[:48].cpu().numpy()
+    n = raw[:16].view("<i4")
+    t0, c0, t1, c1 = (int(x) for x in raw[16:48].view("<u8"))
+    dt = max(t1 - t0, 1)
+    return {"n_ranges": int(n[0]), "n_tiles": int(n[1]), "n_empty": int(n[2]),
+            "first_group_us": dt * 0.01, "sclk_mhz": (c1 - c0) * 100.0 / dt}
 
 
 def _stream(stream):
@@ -129,6 +164,7 @@ def _out_flags(out, flags):
 
 def vd_decode_attn(q, k_pages, v_pages, page_table, seq_lens, out, scale: float, workspace,
                    flags: int = 0, stream=None) -> None:
+    _attn_dtypes(q, k_pages, v_pages, page_table, seq_lens, out)
     B, Hq, Hkv, D, S, maxp = _attn_sizes(q, k_pages, page_table)
     _check(lib().vd_decode_attn(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(page_table),
                                 _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale), maxp,
@@ -145,6 +181,7 @@ def vd_decode_plan(seq_lens, n_q_heads: int, n_kv_heads: int, max_pages_per_seq:
 
 def vd_decode_partial(q, k_pages, v_pages, page_table, seq_lens, out, scale: float, workspace,
                       flags: int = 0, stream=None) -> None:
+    _attn_dtypes(q, k_pages, v_pages, page_table, seq_lens, out)
     B, Hq, Hkv, D, S, maxp = _attn_sizes(q, k_pages, page_table)
     _check(lib().vd_decode_partial(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(page_table),
                                    _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale),
