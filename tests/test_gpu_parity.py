@@ -461,6 +461,42 @@ def test_step_record():
         check_f32(out, ref_of(c), "step record run")
 
 
+@pytest.mark.parametrize("trial", range(8))
+def test_staged_equals_whole_random(trial):
+    """Seeded random shapes, with request counts past one per planning thread
+    (up to 3000) and every KV-head group width: the self-planned kernel and
+    the planner kernel cut the same ranges, so the whole step, the staged
+    calls and the self-planned staged calls agree bit for bit."""
+    rng = np.random.default_rng(3000 + trial)
+    hkv = int(rng.choice([1, 2, 4, 8, 16]))
+    G = int(rng.choice([1, 4, 16])) if hkv < 16 else int(rng.choice([1, 4]))
+    B = (7, 64, 300, 1100, 3000, 1, 300, 1100)[trial]
+    pool = np.array([0, 1, 15, 16, 17, 33, 100, 257, 700])
+    lengths = [int(x) for x in rng.choice(pool, B)]
+    lengths[int(rng.integers(0, B))] = int(rng.integers(1000, 6000))
+    flags = vd.VD_FLAG_RANGE_TILES(int(rng.integers(1, 256))) if rng.random() < 0.3 else 0
+    say("case: staged vs whole, trial %d B %d G %d Hkv %d flags %#x" % (trial, B, G, hkv, flags))
+    c = custom(lengths, hq=G * hkv, hkv=hkv, seed=3100 + trial, fill="zero")
+    d = dev_case(c)
+    Hq, maxp = G * hkv, c["max_pages_per_seq"]
+    whole = run_gpu(d, flags=flags)
+    outs = []
+    for self_plan in (False, True):
+        ws = vd.alloc_workspace(B, Hq, hkv, maxp, flags)
+        o = torch.full(d["q"].shape, float("nan"), dtype=torch.float32, device=DEV)
+        if not self_plan:
+            vd.vd_decode_plan(d["seq_lens"], Hq, hkv, maxp, ws, flags=flags)
+        vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
+                             o, d["scale"], ws,
+                             flags=flags | (vd.VD_FLAG_SELF_PLAN if self_plan else 0))
+        vd.vd_decode_combine(o, hkv, maxp, ws, flags=flags)
+        outs.append(o)
+    torch.cuda.synchronize()
+    for o in outs:
+        assert torch.equal(o.view(torch.int32).cpu(), whole.view(torch.int32).cpu())
+    assert torch.isfinite(whole).all()
+
+
 def test_workspace_reuse_across_steps():
     """One workspace serves steps of different length mixes in a row: what a
     longer step left in it (ranges, boundary records, partials) never leaks
