@@ -82,6 +82,7 @@ constexpr int kPlanThreads = 1024;
 constexpr int kHeadsPerGroup = 4;      // preferred KV heads (waves) per attention workgroup
 constexpr int kAttnWavesPerCU = 4;     // resident attention waves per CU (one per SIMD)
 constexpr int kDeferEntries = 64;      // LDS result entries per wave, over G query heads
+constexpr int kPrePad = 6;             // self-planned prefix in LDS: one pad word per 64 entries
 constexpr int kAttnMaxThreads = 64 * kHeadsPerGroup;
 constexpr int kCombineThreads = 256;
 constexpr int kCombineGroupsPerCU = 4;
@@ -207,29 +208,45 @@ __device__ inline int4 boundary_record(int w, int t, int s, int j, int P, int T,
     return make_int4(s, w0 + s, w1 - w0 + 1, w - w0 - 1);
 }
 
+// Word of entry b of a prefix array in LDS: PAD = 6 skips one word every
+// 64, so that threads walking contiguous runs of entries (one run each)
+// fall in different banks; PAD = 0 is the plain layout.
+template <int PAD>
+__device__ inline int pidx(int b) { return PAD ? b + (b >> PAD) : b; }
+
 // Largest b in [0, B) with pre[b] <= t (pre ascending, pre[B] = T > t): the
 // request holding tile t.
+template <int PAD>
 __device__ inline int find_request(const int *pre, int B, int t)
 {
     int lo = 0, hi = B;
     while (hi - lo > 1) {
         const int mid = (lo + hi) >> 1;
-        if (pre[mid] <= t) lo = mid; else hi = mid;
+        if (pre[pidx<PAD>(mid)] <= t) lo = mid; else hi = mid;
     }
     return lo;
 }
 
-// Descriptor {b, q, j, t} of range w's first tile, and its boundary record.
+// Descriptor {b, q, j, t} of range w, whose first tile t lies in request b,
+// and its boundary record.
+template <int PAD>
+__device__ inline void entry_at(const int *pre, int b, int Hg, int w, int t, int T, int W,
+                                int4 &desc, int4 &rec)
+{
+    const int P = (pre[pidx<PAD>(b + 1)] - pre[pidx<PAD>(b)]) / Hg;
+    const int off = t - pre[pidx<PAD>(b)];
+    const int q = off / P, j = off - q * P;
+    desc = make_int4(b, q, j, t);
+    rec = boundary_record(w, t, b * Hg + q, j, P, T, W);
+}
+
+// The same for any range: the request found by binary search.
+template <int PAD>
 __device__ inline void range_entry(const int *pre, int B, int Hg, int w, int T, int W, int4 &desc,
                                    int4 &rec)
 {
     const int t = range_start(w, T, W);
-    const int b = find_request(pre, B, t);
-    const int P = (pre[b + 1] - pre[b]) / Hg;
-    const int off = t - pre[b];
-    const int q = off / P, j = off - q * P;
-    desc = make_int4(b, q, j, t);
-    rec = boundary_record(w, t, b * Hg + q, j, P, T, W);
+    entry_at<PAD>(pre, find_request<PAD>(pre, B, t), Hg, w, t, T, W, desc, rec);
 }
 
 template <typename T>
@@ -321,7 +338,7 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
             continue;
         }
         int4 desc, rec;
-        range_entry(s_pre, B, Hg, w, T, W, desc, rec);
+        range_entry<0>(s_pre, B, Hg, w, T, W, desc, rec);
         ranges[w] = desc;
         if (w > 0)
             bounds[w] = rec;
@@ -537,9 +554,18 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
     __shared__ int4 s_desc;
     const int nt = blockDim.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, nw = nt >> 6;
     const int B = a.B;
-    for (int b = tid; b < B; b += nt) {
-        const int L = clamped_len(a.seq_lens, b, a.maxp);
-        s_pre[b] = (L + kPage - 1) / kPage * Hg;
+    // eight loads in flight per thread, not one latency per request
+    constexpr int kLoadBatch = 8;
+    for (int b0 = tid; b0 < B; b0 += kLoadBatch * nt) {
+        int L[kLoadBatch];
+#pragma unroll
+        for (int u = 0; u < kLoadBatch; ++u)   // branch-free: indices clamped into the array
+            L[u] = a.seq_lens[min(b0 + u * nt, B - 1)];
+#pragma unroll
+        for (int u = 0; u < kLoadBatch; ++u)
+            if (b0 + u * nt < B)
+                s_pre[pidx<kPrePad>(b0 + u * nt)] =
+                    (L[u] <= 0 ? 0 : (min(L[u], a.maxp * kPage) + kPage - 1) / kPage) * Hg;
     }
     __syncthreads();
     // exclusive prefix of tiles in place; thread tid owns requests [c0, c1).
@@ -548,8 +574,11 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
     const int per = (B + nt - 1) / nt;
     const int c0 = min(B, tid * per), c1 = min(B, c0 + per);
     long long mine = 0;
-    for (int b = c0; b < c1; ++b)
-        mine += (1LL << 32) * (s_pre[b] > 0) + s_pre[b];
+#pragma unroll 8
+    for (int b = c0; b < c1; ++b) {
+        const int n = s_pre[pidx<kPrePad>(b)];
+        mine += (1LL << 32) * (n > 0) + n;
+    }
     const long long inc = wave_inclusive_scan(mine, lane);
     if (lane == 63)
         s_wsum[wv] = inc;
@@ -562,31 +591,45 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
     const long long excl = base + inc - mine;
     const int T = (int)(tot & 0xFFFFFFFFLL), nonempty = (int)(tot >> 32);
     int run = (int)(excl & 0xFFFFFFFFLL);
+#pragma unroll 8
     for (int b = c0; b < c1; ++b) {
-        const int n = s_pre[b];
-        s_pre[b] = run;
+        const int n = s_pre[pidx<kPrePad>(b)];
+        s_pre[pidx<kPrePad>(b)] = run;
         run += n;
     }
     if (tid == 0)
-        s_pre[B] = T;
+        s_pre[pidx<kPrePad>(B)] = T;
     __syncthreads();
 
     const int W = plan_ranges(T, nonempty * Hg, a.forced, a.resident);
     const int2 wr = group_ranges(blockIdx.x, gridDim.x, W);
-    for (int w = wr.x + tid; w < wr.y; w += nt) {
-        int4 desc, rec;
-        range_entry(s_pre, B, Hg, w, T, W, desc, rec);
-        if (w == wr.x)
+    if (wr.x < wr.y) {
+        // the first range: its first tile lies among the requests of one
+        // thread, which walks them (no search)
+        const int t0 = range_start(wr.x, T, W);
+        const int my0 = (int)(excl & 0xFFFFFFFFLL), my1 = my0 + (int)(mine & 0xFFFFFFFFLL);
+        if (my0 <= t0 && t0 < my1) {
+            int b = c0;
+            while (s_pre[pidx<kPrePad>(b + 1)] <= t0)
+                ++b;
+            int4 desc, rec;
+            entry_at<kPrePad>(s_pre, b, Hg, wr.x, t0, T, W, desc, rec);
             s_desc = desc;
-        if (w > 0)
-            a.bounds[w] = rec;
+            if (wr.x > 0)
+                a.bounds[wr.x] = rec;
+        }
+    }
+    for (int w = wr.x + 1 + tid; w < wr.y; w += nt) {
+        int4 desc, rec;
+        range_entry<kPrePad>(s_pre, B, Hg, w, T, W, desc, rec);
+        a.bounds[w] = rec;
     }
     if (blockIdx.x == 0) {
         // header, and the requests without tokens in order: those before c0
         // number c0 minus the non-empty ones
         int pos = c0 - (int)(excl >> 32);
         for (int b = c0; b < c1; ++b)
-            if (s_pre[b + 1] == s_pre[b])
+            if (s_pre[pidx<kPrePad>(b + 1)] == s_pre[pidx<kPrePad>(b)])
                 a.empty[pos++] = b;
         if (tid == 0) {
             a.hdr->n_ranges = W;
@@ -1284,8 +1327,9 @@ int log2_pow2(int x)
 std::atomic<int> g_resident[kMaxDevices][5][3][3];
 
 // The self-planned prologue keeps the tile prefix of up to kMaxSeqs requests
-// in the result-entry space of one wave (the smallest case: G = 16).
-static_assert((kDeferEntries / 16) * (16 * kHeadDim * 4 + 16 * 8 + 2 * 4) >= 4 * (kMaxSeqs + 1),
+// (padded) in the result-entry space of one wave (the smallest case: G = 16).
+static_assert((kDeferEntries / 16) * (16 * kHeadDim * 4 + 16 * 8 + 2 * 4) >=
+                  4 * (kMaxSeqs + 1 + ((kMaxSeqs + 1) >> kPrePad) + 1),
               "request prefix does not fit the attention kernel's LDS");
 
 // Dynamic LDS of an attention workgroup: per wave, kDeferEntries / G piece
