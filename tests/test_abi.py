@@ -46,6 +46,9 @@ def test_workspace_size_rules():
     assert ws(256, 30, 8, 128, 16, 1024) == 0              # Hq % Hkv != 0
     assert ws(8193, 32, 8, 128, 16, 16) == 0               # too many requests
     assert ws(4, 32, 8, 128, 16, 63, 1 << 5) == 0          # unknown flag bit
+    # planning in the attention kernel needs no other workspace
+    assert ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_SELF_PLAN) == ws(4, 32, 8, 128, 16, 63)
+    assert ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_SELF_PLAN | vd.VD_FLAG_OUT_F32) == ws(4, 32, 8, 128, 16, 63)
     # one tile per range: up to one partial per (page, KV head) plus one per segment
     small = ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_RANGE_TILES(1))
     assert small >= (4 * 63 * 8 + 4 * 8) * 4 * 128 * 4
@@ -154,3 +157,14 @@ def test_product_does_not_reference_oracle():
     with open(os.path.join(pkg, "libvdecode.so"), "rb") as fh:
         blob = fh.read()
     assert b"vdo_" not in blob and b"libvdo_oracle" not in blob
+
+
+def test_binding_constants_match_header():
+    """The binding's status codes and flags are the header's."""
+    hdr = open(os.path.join(ROOT, "include", "vdecode.h")).read()
+    for name, val in re.findall(r"#define (VD_FLAG_\w+) \(1u << (\d+)\)", hdr):
+        assert getattr(vd, name) == 1 << int(val), name
+    for name, val in re.findall(r"(VD_(?:SUCCESS|ERROR_\w+)) = (\d+)", hdr):
+        assert getattr(vd, name) == int(val), name
+    assert vd.VD_FLAG_RANGE_SHIFT == int(re.search(r"#define VD_FLAG_RANGE_SHIFT (\d+)u", hdr).group(1))
+
