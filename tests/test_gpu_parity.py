@@ -457,7 +457,7 @@ def test_step_record():
         assert n[1] == tiles and n[2] == 1 and 1 <= n[0] <= tiles
         assert t1 > t0 and c1 > c0
         assert us_first <= 1.5 * us_event + 20.0
-        assert 50.0 <= mhz <= 3500.0
+        assert 10.0 <= mhz <= 3500.0   # the clock may still be ramping up from idle
         check_f32(out, ref_of(c), "step record run")
 
 
