@@ -14,7 +14,10 @@ surface written by ``bench.py --surface``).  CPU only; it consumes the
 measurements and launches nothing.  XGBoost is not available in this
 environment, so the boosted model is scikit-learn's histogram gradient
 boosting with the same objective, rate, depth, round budget and patience
-(it has no row/column subsampling).
+(it has no row/column subsampling).  Its leaves may hold a single sample, as
+XGBoost's default minimum child weight of one allows; scikit-learn's own
+default of twenty samples per leaf leaves almost no splits on a surface of
+about a hundred points.
 """
 from __future__ import annotations
 
@@ -73,7 +76,7 @@ def fit_boosted(n_req, n_kv, t, random_state: int = 42):
     model = HistGradientBoostingRegressor(
         loss="absolute_error", learning_rate=0.1, max_iter=1000, max_depth=6,
         early_stopping=True, n_iter_no_change=200, validation_fraction=0.2,
-        random_state=random_state)
+        min_samples_leaf=1, random_state=random_state)
     model.fit(X, np.asarray(t, float))
     return model
 

@@ -36,3 +36,19 @@ def test_holdout_reports_both():
     t = 0.02 * n_req + 6.25e-4 * n_kv + 21.5
     r = lm.holdout_mae(n_req, n_kv, t)
     assert r["linear_mae_us"] < 1e-6 and r["n_test"] + r["n_train"] == 60
+
+
+def test_boosted_interpolates_a_sparse_surface():
+    """About a hundred points spanning three orders of magnitude, as the
+    measured surface: trees with single-sample leaves (XGBoost's default
+    minimum child weight) interpolate held-out points within a few percent;
+    leaves of twenty samples would not split this grid at all."""
+    n_req, n_kv = grid()
+    t = 0.02 * n_req + 6.25e-4 * n_kv + 21.5
+    rng = np.random.default_rng(1)
+    idx = rng.permutation(t.size)
+    te, tr = idx[:15], idx[15:]
+    m = lm.fit_boosted(n_req[tr], n_kv[tr], t[tr])
+    pred = m.predict(np.stack([n_req[te], n_kv[te]], 1))
+    assert np.median(np.abs(pred - t[te]) / t[te]) < 0.1
+
