@@ -44,6 +44,33 @@ class LinearFit:
         return kv_bytes_per_token / (self.d * 1e-6) / 1e9
 
 
+@dataclass
+class ClockScaledFit:
+    """Per-clock coefficients of Eq. pred-itl from one measured clock: the
+    paper fits c_f, d_f, e_f per GPU frequency f (Sec. 5.4); with the
+    frequency relation T ~ f^-beta (Sec. 3.2, Eq. t-alpha-beta) measured for
+    this kernel, T_f = T_f0 * (f0 / f)^beta scales all three alike."""
+    base: LinearFit
+    f0_mhz: float
+    beta: float
+
+    def at(self, f_mhz: float) -> LinearFit:
+        k = (self.f0_mhz / float(f_mhz)) ** self.beta
+        b = self.base
+        return LinearFit(b.c * k, b.d * k, b.e * k, b.r2, b.mae * k)
+
+    def predict(self, n_req, n_kv, f_mhz):
+        return self.at(f_mhz).predict(n_req, n_kv)
+
+
+def fit_beta(f_mhz, t) -> float:
+    """beta of T ~ f^-beta by least squares on ln T = a - beta ln f."""
+    f, t = np.asarray(f_mhz, float), np.asarray(t, float)
+    A = np.stack([np.ones_like(f), np.log(f)], axis=1)
+    (_, b), *_ = np.linalg.lstsq(A, np.log(t), rcond=None)
+    return float(-b)
+
+
 def load_surface(path: str, n_q_heads: int | None = 32, column: str = "us_step"):
     """Rows of a latency-surface CSV as (n_req, n_kv, step time) arrays;
     `column` picks the eager step time (us_step) or the graph replay time

@@ -52,3 +52,18 @@ def test_boosted_interpolates_a_sparse_surface():
     pred = m.predict(np.stack([n_req[te], n_kv[te]], 1))
     assert np.median(np.abs(pred - t[te]) / t[te]) < 0.1
 
+
+def test_clock_scaled_fit():
+    """beta recovered from T ~ f^-beta, and per-clock coefficients scaled by
+    (f0 / f)^beta (the same model at its own clock returns itself)."""
+    f = np.linspace(1400, 2400, 40)
+    t = 250.0 * (2400.0 / f) ** 0.095
+    beta = lm.fit_beta(f, t)
+    assert abs(beta - 0.095) < 1e-9
+    n_req, n_kv = grid()
+    base = lm.fit_linear(n_req, n_kv, 0.02 * n_req + 6.25e-4 * n_kv + 21.5)
+    m = lm.ClockScaledFit(base, 2400.0, beta)
+    assert np.allclose(m.predict(n_req, n_kv, 2400.0), base.predict(n_req, n_kv))
+    slow = m.at(1200.0)
+    assert abs(slow.d / base.d - 2.0 ** 0.095) < 1e-12 and abs(slow.e / base.e - 2.0 ** 0.095) < 1e-12
+
