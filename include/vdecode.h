@@ -87,9 +87,10 @@ const char *vd_status_string(int status);
 
 /*
  * Step record.  Every attention launch (vd_decode_attn, vd_decode_partial,
- * vd_decode_gather) leaves one at offset 0 of its workspace, written by the
- * kernel's first workgroup when it finishes: the plan's sizes, and two
- * device counters read when that workgroup starts and ends.  The counters
+ * vd_decode_gather) leaves one at offset 0 of its workspace: the plan's
+ * sizes (from the planner, or from the self-planning kernel's first
+ * workgroup), and two device counters that the kernel's first workgroup
+ * reads when it starts and when it ends.  The counters
  * give the shader clock the step ran at, the quantity the paper's
  * frequency-latency relation is stated in (Sec. 3.2, Eq. t-alpha-beta):
  *   t_start, t_end      the constant-rate real-time counter (100 MHz on
@@ -137,9 +138,10 @@ int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
 
 /*
  * Stage 1 of 3: lay every (page, KV head) tile of the step out in one sequence
- * (request, KV head, page order) and cut it into as many equal ranges as the
- * device runs waves at once, so every wave streams the same number of tiles
- * whatever the length mix; write that plan into the workspace.  Depends only
+ * (request, KV head, page order) and cut it into equal ranges, as many as
+ * (or a multiple of) the attention workgroups the device runs at once (fewer
+ * for small steps), so every wave streams the same number of tiles whatever
+ * the length mix; write that plan into the workspace.  Depends only
  * on seq_lens and the sizes, so one plan serves every layer of a decode step.
  * Not needed before a vd_decode_partial with VD_FLAG_SELF_PLAN, which cuts
  * the same ranges itself.
@@ -179,7 +181,7 @@ int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads,
                       hipStream_t stream);
 
 /*
- * Copy-through check of the gather: plans like vd_decode_attn, runs the
+ * Copy-through check of the gather: plans with the planner kernel, runs the
  * attention kernel's own page-table walk, K/V loads, tail masking and
  * matrix-operand assembly, and writes every cached K and V row it assembled
  * to k_out / v_out (bf16 [sum_b L_b][n_kv_heads][head_dim], requests in order,
