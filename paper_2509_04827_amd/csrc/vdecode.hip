@@ -167,31 +167,40 @@ __device__ inline int clamped_len(const int32_t *seq_lens, int b, int maxp)
 // one to a range rather than several in a row), up to R ranges; past that W
 // is a multiple of R with at most kMaxRangeTiles tiles per range.  W <= T,
 // so no range is empty.
+// (All sizes here are below 2^31, so the 32-bit quotients are exact; unsigned
+// arithmetic keeps the divisions short.)
+__device__ inline unsigned ceil_div_u(unsigned a, unsigned b) { return (a + b - 1) / b; }
+
 __device__ inline int plan_ranges(int T, int nseg, int forced, int R)
 {
     if (T == 0)
         return 0;
+    const unsigned t = (unsigned)T;
     if (forced > 0)
-        return (int)ceil_div_ll(T, forced);
-    const int m = (int)std::min<long long>(kMinRangeTiles, ceil_div_ll(T, std::max(nseg, 1)));
-    const long long W = std::min<long long>(R, ceil_div_ll(T, m));
-    return W == R ? (int)(R * ceil_div_ll(T, (long long)kMaxRangeTiles * R)) : (int)W;
+        return (int)ceil_div_u(t, (unsigned)forced);
+    const unsigned m = min((unsigned)kMinRangeTiles, ceil_div_u(t, (unsigned)max(nseg, 1)));
+    const unsigned W = min((unsigned)R, ceil_div_u(t, m));
+    return W == (unsigned)R ? (int)((unsigned)R * ceil_div_u(t, (unsigned)kMaxRangeTiles * R)) : (int)W;
 }
 
 // first tile of range w: floor(w * T / W)
-__device__ inline int range_start(int w, int T, int W) { return (int)((long long)w * T / W); }
+__device__ inline int range_start(int w, int T, int W)
+{
+    return (int)((unsigned long long)(unsigned)w * (unsigned)T / (unsigned)W);
+}
 
 // range holding tile t
 __device__ inline int range_of(long long t, long long T, long long W)
 {
-    return (int)(((t + 1) * W - 1) / T);
+    return (int)(((unsigned long long)(t + 1) * (unsigned long long)W - 1) / (unsigned long long)T);
 }
 
 // Ranges [lo, hi) of workgroup g of n: consecutive, as equal in number as
 // they can be.
 __device__ inline int2 group_ranges(int g, int n, int W)
 {
-    return make_int2((int)((long long)g * W / n), (int)((long long)(g + 1) * W / n));
+    const unsigned long long w = (unsigned)W, u = (unsigned)n;
+    return make_int2((int)((unsigned)g * w / u), (int)((unsigned)(g + 1) * w / u));
 }
 
 // Boundary record of range w >= 1, whose first tile t is page j of segment
@@ -364,7 +373,7 @@ struct AttnArgs {
     float2 *part_ml;
     float *part_acc;
     int Hq, Hkv, HW, pt_stride, maxp;
-    int B, forced, resident;        // self-planned: requests, forced range length, R
+    int B, forced, resident;        // requests, forced range length (self-planned); R = grid size
     float scale_log2;
 };
 
@@ -552,7 +561,9 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
 {
     __shared__ long long s_wsum[kHeadsPerGroup];
     __shared__ int4 s_desc;
-    const int nt = blockDim.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, nw = nt >> 6;
+    // the launch shape comes from the arguments: reading blockDim / gridDim
+    // costs a load from the dispatch packet at kernel start
+    const int nt = 64 * a.HW, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, nw = a.HW;
     const int B = a.B;
     // eight loads in flight per thread, not one latency per request
     constexpr int kLoadBatch = 8;
@@ -562,10 +573,11 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
         for (int u = 0; u < kLoadBatch; ++u)   // branch-free: indices clamped into the array
             L[u] = a.seq_lens[min(b0 + u * nt, B - 1)];
 #pragma unroll
-        for (int u = 0; u < kLoadBatch; ++u)
-            if (b0 + u * nt < B)
-                s_pre[pidx<kPrePad>(b0 + u * nt)] =
-                    (L[u] <= 0 ? 0 : (min(L[u], a.maxp * kPage) + kPage - 1) / kPage) * Hg;
+        for (int u = 0; u < kLoadBatch; ++u) {   // past the end: a 0 into slot B, set later
+            const int b = b0 + u * nt;
+            const int n = (L[u] <= 0 ? 0 : (min(L[u], a.maxp * kPage) + kPage - 1) / kPage) * Hg;
+            s_pre[pidx<kPrePad>(min(b, B))] = b < B ? n : 0;
+        }
     }
     __syncthreads();
     // exclusive prefix of tiles in place; thread tid owns requests [c0, c1).
@@ -602,7 +614,7 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
     __syncthreads();
 
     const int W = plan_ranges(T, nonempty * Hg, a.forced, a.resident);
-    const int2 wr = group_ranges(blockIdx.x, gridDim.x, W);
+    const int2 wr = group_ranges(blockIdx.x, a.resident, W);
     if (wr.x < wr.y) {
         // the first range: its first tile lies among the requests of one
         // thread, which walks them (no search)
@@ -882,7 +894,7 @@ __device__ inline void attn_body(const AttnArgs &a)
     } else {
         const const_i32p hdr = (const const_i32p)a.hdr;
         const int W = hdr[0], T = hdr[1];
-        const int2 wr = group_ranges(blockIdx.x, gridDim.x, W);
+        const int2 wr = group_ranges(blockIdx.x, a.resident, W);
         if (wr.x >= wr.y)
             return;
         const const_i32p rg = (const_i32p)(a.ranges + wr.x);
@@ -1035,6 +1047,7 @@ struct CombineArgs {
     const float2 *part_ml;
     const float *part_acc;
     int Hq, Hkv, G, HW;
+    int grid;               // workgroups launched (not read from the dispatch packet)
 };
 
 // Work items, strided over the workgroups: one per range boundary, then one
@@ -1115,7 +1128,7 @@ combine_kernel(const CombineArgs a)
     const int G = a.G, HW = a.HW, Hg = a.Hkv / a.HW;
     const int rows = HW * G;
     const int n_bounds = W > 1 ? W - 1 : 0;
-    for (int item = blockIdx.x; item < n_bounds + n_empty; item += gridDim.x) {
+    for (int item = blockIdx.x; item < n_bounds + n_empty; item += a.grid) {
         if (item >= n_bounds) {
             const int b = a.empty[item - n_bounds];
             for (int u = threadIdx.x; u < a.Hq * (kHeadDim / 4); u += kCombineThreads)
@@ -1465,6 +1478,7 @@ int enqueue_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, cons
     // work items: fewer than one per range plus one per request
     const long long items = lay.cap + (long long)num_seqs;
     const dim3 grid((unsigned)std::min<long long>((long long)cus * kCombineGroupsPerCU, items));
+    c.grid = (int)grid.x;
     if (flags & VD_FLAG_OUT_F32)
         hipLaunchKernelGGL(combine_kernel<MODE_F32>, grid, dim3(kCombineThreads), 0, stream, c);
     else
