@@ -258,6 +258,22 @@ __device__ inline void range_entry(const int *pre, int B, int Hg, int w, int T, 
     entry_at<PAD>(pre, find_request<PAD>(pre, B, t), Hg, w, t, T, W, desc, rec);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave on DPP: Hillis-Steele
+// within rows of 16 lanes (row_shr 1, 2, 4, 8; lanes shifted in from outside
+// the row read 0), then lane 15 of rows 0 and 2 added into rows 1 and 3
+// (row_bcast:15) and lane 31 into rows 2 and 3 (row_bcast:31).  Six VALU
+// adds, no LDS round trip.
+__device__ inline unsigned wave_scan_dpp(unsigned x)
+{
+    x += (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xf, 0xf, true);
+    x += (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xf, 0xf, true);
+    x += (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xf, 0xf, true);
+    x += (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xf, 0xf, true);
+    x += (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xa, 0xf, false);
+    x += (unsigned)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xc, 0xf, false);
+    return x;
+}
+
 template <typename T>
 __device__ inline T wave_inclusive_scan(T x, int lane)
 {
@@ -559,7 +575,7 @@ struct PieceWalk {
 // Returns false when the workgroup has no range.
 __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWalk &walk)
 {
-    __shared__ long long s_wsum[kHeadsPerGroup];
+    __shared__ uint2 s_wsum[kHeadsPerGroup];
     __shared__ int4 s_desc;
     // the launch shape comes from the arguments: reading blockDim / gridDim
     // costs a load from the dispatch packet at kernel start
@@ -581,28 +597,31 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
     }
     __syncthreads();
     // exclusive prefix of tiles in place; thread tid owns requests [c0, c1).
-    // The scan carries (non-empty requests << 32) + tiles: both sums at once
-    // (tiles < 2^31, so the low half never carries).
+    // Two scans at once: tiles and non-empty requests.
     const int per = (B + nt - 1) / nt;
     const int c0 = min(B, tid * per), c1 = min(B, c0 + per);
-    long long mine = 0;
+    unsigned my_t = 0, my_n = 0;
 #pragma unroll 8
     for (int b = c0; b < c1; ++b) {
         const int n = s_pre[pidx<kPrePad>(b)];
-        mine += (1LL << 32) * (n > 0) + n;
+        my_t += (unsigned)n;
+        my_n += n > 0;
     }
-    const long long inc = wave_inclusive_scan(mine, lane);
+    const unsigned inc_t = wave_scan_dpp(my_t), inc_n = wave_scan_dpp(my_n);
     if (lane == 63)
-        s_wsum[wv] = inc;
+        s_wsum[wv] = make_uint2(inc_t, inc_n);
     __syncthreads();
-    long long base = 0, tot = 0;
+    unsigned base_t = 0, base_n = 0, tot_t = 0, tot_n = 0;
     for (int x = 0; x < nw; ++x) {
-        base += x < wv ? s_wsum[x] : 0;
-        tot += s_wsum[x];
+        const uint2 v = s_wsum[x];
+        base_t += x < wv ? v.x : 0u;
+        base_n += x < wv ? v.y : 0u;
+        tot_t += v.x;
+        tot_n += v.y;
     }
-    const long long excl = base + inc - mine;
-    const int T = (int)(tot & 0xFFFFFFFFLL), nonempty = (int)(tot >> 32);
-    int run = (int)(excl & 0xFFFFFFFFLL);
+    const int T = (int)tot_t, nonempty = (int)tot_n;
+    const int excl_t = (int)(base_t + inc_t - my_t), excl_n = (int)(base_n + inc_n - my_n);
+    int run = excl_t;
 #pragma unroll 8
     for (int b = c0; b < c1; ++b) {
         const int n = s_pre[pidx<kPrePad>(b)];
@@ -619,7 +638,7 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
         // the first range: its first tile lies among the requests of one
         // thread, which walks them (no search)
         const int t0 = range_start(wr.x, T, W);
-        const int my0 = (int)(excl & 0xFFFFFFFFLL), my1 = my0 + (int)(mine & 0xFFFFFFFFLL);
+        const int my0 = excl_t, my1 = excl_t + (int)my_t;
         if (my0 <= t0 && t0 < my1) {
             int b = c0;
             while (s_pre[pidx<kPrePad>(b + 1)] <= t0)
@@ -639,7 +658,7 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
     if (blockIdx.x == 0) {
         // header, and the requests without tokens in order: those before c0
         // number c0 minus the non-empty ones
-        int pos = c0 - (int)(excl >> 32);
+        int pos = c0 - excl_n;
         for (int b = c0; b < c1; ++b)
             if (s_pre[pidx<kPrePad>(b + 1)] == s_pre[pidx<kPrePad>(b)])
                 a.empty[pos++] = b;
