@@ -145,42 +145,43 @@ def latency_surface(outdir: str, iters: int = 10, warmup: int = 3):
         en.record(stream)
         torch.cuda.synchronize()
         us_step = st.elapsed_time(en) * 1e3 / iters
-        # the attention kernel alone: the same launches back to back (see main())
-        ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        ea.record(stream)
-        for _ in range(iters):
-            vd.vd_decode_partial(q, kp, vp, ptd, sl, out, scale, ws, flags=vd.VD_FLAG_SELF_PLAN,
-                                 stream=stream)
-        eb.record(stream)
-        torch.cuda.synchronize()
-        us_attn = ea.elapsed_time(eb) * 1e3 / iters
-        # the same step captured into a HIP graph and replayed: no host launch
-        # cost per kernel, so small steps show the device-side floor
+        # device time per call: `iters` calls captured into one HIP graph and
+        # replayed, so the host launches nothing per call and small steps show
+        # the device's own time (kernels and the gaps between them), not the
+        # binding's call rate; the first replay is a warm-up
         side = torch.cuda.Stream()
         side.wait_stream(stream)
         with torch.cuda.stream(side):
             vd.vd_decode_attn(q, kp, vp, ptd, sl, out, scale, ws)
         stream.wait_stream(side)
         torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            vd.vd_decode_attn(q, kp, vp, ptd, sl, out, scale, ws)
-        for _ in range(warmup):
+
+        def graph_us(call, reps=3):
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                for _ in range(iters):
+                    call()
             graph.replay()
-        torch.cuda.synchronize()
-        st.record(stream)
-        for _ in range(iters):
-            graph.replay()
-        en.record(stream)
-        torch.cuda.synchronize()
-        us_graph = st.elapsed_time(en) * 1e3 / iters
-        del graph
+            torch.cuda.synchronize()
+            st.record(stream)
+            for _ in range(reps):
+                graph.replay()
+            en.record(stream)
+            torch.cuda.synchronize()
+            del graph
+            return st.elapsed_time(en) * 1e3 / (reps * iters)
+
+        us_graph = graph_us(lambda: vd.vd_decode_attn(q, kp, vp, ptd, sl, out, scale, ws))
+        # the attention kernel alone (the launches vd_decode_attn makes first)
+        us_attn = graph_us(lambda: vd.vd_decode_partial(q, kp, vp, ptd, sl, out, scale, ws,
+                                                        flags=vd.VD_FLAG_SELF_PLAN))
         n_kv = int(lens.sum())
         kvb = n_kv * Hkv * D * 2 * 2
         rows.append(dict(law=law, n_q_heads=Hq, n_req=B, tokens_per_req=int(round(lens.mean())),
                          n_kv=n_kv, us_step=round(us_step, 2), us_attn=round(us_attn, 2),
                          us_step_graph=round(us_graph, 2),
-                         kv_gbs_step=round(kvb / us_step / 1e3, 1)))
+                         kv_gbs_step=round(kvb / us_step / 1e3, 1),
+                         kv_gbs_graph=round(kvb / us_graph / 1e3, 1)))
         print("surface %-8s Hq %2d B %4d L %6d N_kv %8d  step %9.2f us  graph %9.2f us  attn %9.2f us  %7.1f GB/s"
               % (law, Hq, B, lens.mean(), n_kv, us_step, us_graph, us_attn, kvb / us_step / 1e3),
               file=sys.stderr, flush=True)

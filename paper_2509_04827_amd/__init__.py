@@ -75,11 +75,19 @@ def lib() -> ctypes.CDLL:
         L.vd_decode_plan.argtypes = [P, I, I, I, I, I, I, P, Z, U, P]
         L.vd_decode_combine.argtypes = [P, I, I, I, I, I, I, P, Z, U, P]
         L.vd_decode_gather.argtypes = [P, P, P, P, P, P, I, I, I, I, I, P, Z, P]
+        L.vd_kv_append.argtypes = [P, P, P, P, P, P, I, I, I, I, I, P]
+        L.vd_gemm_workspace_size.argtypes = [I, I, I, U]
+        L.vd_gemm_workspace_size.restype = Z
+        L.vd_gemm_bf16.argtypes = [P, P, P, I, I, I, P, Z, U, P]
         L.vd_stream_read.argtypes = [P, Z, P, I, P]
         for n in ("vd_decode_attn", "vd_decode_partial", "vd_decode_plan", "vd_decode_combine",
-                  "vd_decode_gather", "vd_kv_append", "vd_gemm_workspace_size", "vd_gemm_bf16",
-           "vd_stream_read"):
+                  "vd_decode_gather", "vd_kv_append", "vd_gemm_bf16", "vd_stream_read"):
             getattr(L, n).restype = I
+        # every export has a prototype: pointers travel as plain ints, which
+        # ctypes would otherwise pass as 32-bit C ints
+        missing = [n for n in EXPORTS if getattr(L, n).argtypes is None]
+        if missing:
+            raise RuntimeError("no ctypes prototype for %s" % ", ".join(missing))
         _lib = L
     return _lib
 
@@ -105,14 +113,15 @@ def alloc_workspace(num_seqs, n_q_heads, n_kv_heads, max_pages_per_seq, flags=0,
 
 
 def _ptr(t):
-    """Device address of a tensor the kernels read or write as a dense array."""
+    """Device address of a tensor the kernels read or write as a dense array
+    (an int, which ctypes passes as void *)."""
     if t is None:
         return None
+    if t.is_cuda and t.is_contiguous():
+        return t.data_ptr()
     if not t.is_contiguous():
         raise ValueError("libvdecode needs contiguous tensors (got strides %s)" % (t.stride(),))
-    if t.device.type != "cuda":
-        raise ValueError("libvdecode needs device tensors (got one on %s)" % t.device)
-    return ctypes.c_void_p(t.data_ptr())
+    raise ValueError("libvdecode needs device tensors (got one on %s)" % t.device)
 
 
 def _dtype(t, allowed, what):
@@ -120,12 +129,20 @@ def _dtype(t, allowed, what):
         raise ValueError("%s must be %s (got %s)" % (what, " or ".join(map(str, allowed)), t.dtype))
 
 
+_BF16, _I32, _F32 = torch.bfloat16, torch.int32, torch.float32
+
+
 def _attn_dtypes(q, k_pages, v_pages, page_table, seq_lens, out):
+    # one comparison chain on the common path; the per-tensor checks name the culprit
+    if (q.dtype is _BF16 and k_pages.dtype is _BF16 and v_pages.dtype is _BF16
+            and page_table.dtype is _I32 and seq_lens.dtype is _I32
+            and (out.dtype is _BF16 or out.dtype is _F32)):
+        return
     for t, n in ((q, "q"), (k_pages, "k_pages"), (v_pages, "v_pages")):
-        _dtype(t, (torch.bfloat16,), n)
-    _dtype(page_table, (torch.int32,), "page_table")
-    _dtype(seq_lens, (torch.int32,), "seq_lens")
-    _dtype(out, (torch.bfloat16, torch.float32), "out")
+        _dtype(t, (_BF16,), n)
+    _dtype(page_table, (_I32,), "page_table")
+    _dtype(seq_lens, (_I32,), "seq_lens")
+    _dtype(out, (_BF16, _F32), "out")
 
 
 def step_info(workspace) -> dict:
@@ -142,9 +159,13 @@ def step_info(workspace) -> dict:
 
 
 def _stream(stream):
+    """hipStream_t of `stream`: torch's current stream when None, a
+    torch.cuda.Stream, or a raw handle (int) taken from one."""
     if stream is None:
-        stream = torch.cuda.current_stream()
-    return ctypes.c_void_p(stream.cuda_stream)
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
 
 
 def _check(st, where):
@@ -159,7 +180,7 @@ def _attn_sizes(q, k_pages, page_table):
 
 
 def _out_flags(out, flags):
-    return flags | (VD_FLAG_OUT_F32 if out.dtype == torch.float32 else 0)
+    return flags | (VD_FLAG_OUT_F32 if out.dtype is _F32 else 0)
 
 
 def vd_decode_attn(q, k_pages, v_pages, page_table, seq_lens, out, scale: float, workspace,

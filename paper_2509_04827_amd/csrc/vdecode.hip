@@ -76,7 +76,6 @@ constexpr int kHeadDim = 128;
 constexpr int kPage = 16;
 constexpr int kMaxSeqs = 8192;         // every request's tile offset fits in LDS when planning
 constexpr int kMaxRangeTiles = 512;    // eight 64-entry page-id windows per piece
-constexpr int kMinRangeTiles = 4;      // small steps: ranges of at least min(this, mean segment) tiles
 constexpr int kMaxResidentGroups = 4096;
 constexpr int kPlanThreads = 1024;
 constexpr int kHeadsPerGroup = 4;      // preferred KV heads (waves) per attention workgroup
@@ -84,8 +83,8 @@ constexpr int kAttnWavesPerCU = 4;     // resident attention waves per CU (one p
 constexpr int kDeferEntries = 64;      // LDS result entries per wave, over G query heads
 constexpr int kPrePad = 6;             // self-planned prefix in LDS: one pad word per 64 entries
 constexpr int kAttnMaxThreads = 64 * kHeadsPerGroup;
-constexpr int kCombineThreads = 256;
-constexpr int kCombineGroupsPerCU = 4;
+constexpr int kCombineThreads = 512;
+constexpr int kCombineGroupsPerCU = 2;
 constexpr float kLog2e = 1.4426950408889634f;
 // Lazy rescaling: the running max is only raised when a new score exceeds it
 // by more than this (log2 units), so weights stay below 2^8 and acc/l never
@@ -153,7 +152,6 @@ inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced)
 // The same arithmetic serves the planner kernel (staged API) and the
 // attention kernel's own prologue (whole step), so both cut identical ranges.
 constexpr int kPlanPerThread = kMaxSeqs / kPlanThreads;   // requests per planner thread
-constexpr int kShortMerge = 8;         // segments with more pieces are merged per query head
 
 __device__ inline int clamped_len(const int32_t *seq_lens, int b, int maxp)
 {
@@ -161,26 +159,24 @@ __device__ inline int clamped_len(const int32_t *seq_lens, int b, int maxp)
     return L <= 0 ? 0 : min(L, maxp * kPage);
 }
 
-// Number of ranges W for T tiles in nseg non-empty segments.  A forced
-// length c gives ceil(T / c).  Otherwise ranges hold at least m tiles, m the
-// mean segment length clamped to [1, kMinRangeTiles] (so short segments go
-// one to a range rather than several in a row), up to R ranges; past that W
-// is a multiple of R with at most kMaxRangeTiles tiles per range.  W <= T,
-// so no range is empty.
+// Number of ranges W for T tiles.  A forced length c gives ceil(T / c).
+// Otherwise a step of at most R tiles gets one range per tile (as many
+// workgroups stream as there are tiles, and the combine merges the pieces in
+// one round of loads, which costs less than a longer chain of pages per
+// wave); past that W is a multiple of R with at most kMaxRangeTiles tiles per
+// range.  W <= T, so no range is empty.
 // (All sizes here are below 2^31, so the 32-bit quotients are exact; unsigned
 // arithmetic keeps the divisions short.)
 __device__ inline unsigned ceil_div_u(unsigned a, unsigned b) { return (a + b - 1) / b; }
 
-__device__ inline int plan_ranges(int T, int nseg, int forced, int R)
+__device__ inline int plan_ranges(int T, int forced, int R)
 {
     if (T == 0)
         return 0;
     const unsigned t = (unsigned)T;
     if (forced > 0)
         return (int)ceil_div_u(t, (unsigned)forced);
-    const unsigned m = min((unsigned)kMinRangeTiles, ceil_div_u(t, (unsigned)max(nseg, 1)));
-    const unsigned W = min((unsigned)R, ceil_div_u(t, m));
-    return W == (unsigned)R ? (int)((unsigned)R * ceil_div_u(t, (unsigned)kMaxRangeTiles * R)) : (int)W;
+    return T < R ? T : (int)((unsigned)R * ceil_div_u(t, (unsigned)kMaxRangeTiles * R));
 }
 
 // first tile of range w: floor(w * T / W)
@@ -351,7 +347,7 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
     }
     __syncthreads();
     const int T = s_pre[B];
-    const int W = plan_ranges(T, (B - s_nempty) * Hg, forced, resident_groups);
+    const int W = plan_ranges(T, forced, resident_groups);
 
     // range starts {b, q, j, t} (range W is the end sentinel) and the
     // boundary records of ranges 1 .. W-1
@@ -632,7 +628,7 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
         s_pre[pidx<kPrePad>(B)] = T;
     __syncthreads();
 
-    const int W = plan_ranges(T, nonempty * Hg, a.forced, a.resident);
+    const int W = plan_ranges(T, a.forced, a.resident);
     const int2 wr = group_ranges(blockIdx.x, a.resident, W);
     if (wr.x < wr.y) {
         // the first range: its first tile lies among the requests of one
@@ -1067,22 +1063,23 @@ struct CombineArgs {
     const float *part_acc;
     int Hq, Hkv, G, HW;
     int grid;               // workgroups launched (not read from the dispatch packet)
+    int cap;                // entries of bounds
 };
 
 // Work items, strided over the workgroups: one per range boundary, then one
 // per request without tokens (its output rows are zeros).  A boundary
 // inside a segment names that segment's first partial slot and piece count n
-// and its own index i among the segment's n - 1 inner boundaries:
-//   n <= kShortMerge: the first inner boundary (i = 0) merges the segment;
-//     its HW * G query heads x 32 float4 chunks of head_dim are spread over
-//     the threads, each merging all pieces of its chunk with the loads of a
-//     block of pieces issued before use;
-//   larger n: inner boundary i merges query heads i, i + n - 1, ...; per
-//     head 32 chunks x kCombineLanes piece lanes, lane l merging pieces l,
-//     l + lanes, ..., then the lanes' (max, normaliser, accumulator) merged
-//     in LDS.
+// and its own index i among the segment's n - 1 inner boundaries.  Boundary
+// i merges query-head rows i, i + n - 1, ... of the segment's HW * G rows,
+// so the rows are spread over the workgroups of all its boundaries.  Each
+// output chunk (row, 4 floats of head_dim) gets P adjacent lanes, P a power
+// of two no larger than n or kCombineMaxLanes, as many as the threads allow;
+// lane p merges pieces p, p + P, ... (the loads of four pieces issued
+// before use), then the P lanes' (max, normaliser, accumulator) are merged
+// by lane shuffles within the wave.  A small step's merge is then one round of loads.
 // Merging is a running log-sum-exp in the exp2 domain.
-constexpr int kCombineLanes = kCombineThreads / (kHeadDim / 4);
+constexpr int kChunks = kHeadDim / 4;     // float4 chunks of one query head's output
+constexpr int kCombineMaxLanes = 16;
 constexpr int kCombineUnroll = 4;
 
 struct Lse {
@@ -1136,69 +1133,78 @@ __device__ inline void store_out(const CombineArgs &a, size_t dst, f32x4 o)
     }
 }
 
+// The rows of one segment that boundary record `rec` assigns to this
+// workgroup.
+template <int MODE>
+__device__ inline void merge_boundary(const CombineArgs &a, int4 rec, int rows, int Hg)
+{
+    const int s = rec.x, first = rec.y, n = rec.z, i = rec.w;
+    if (n == 0 || i >= rows)   // a range that starts its segment, or no row left here
+        return;
+    const int b = s / Hg, q = s - b * Hg;
+    const int nb = n - 1;                     // inner boundaries of the segment, n >= 2
+    const int outs = ((rows - 1 - i) / nb + 1) * kChunks;
+    int lg = 0;   // P = 2^lg lanes per chunk
+    while ((1 << lg) < kCombineMaxLanes && (2 << lg) <= n && (2 << lg) * outs <= kCombineThreads)
+        ++lg;
+    const int P = 1 << lg, G = a.G;
+    for (int u = threadIdx.x; u - (int)threadIdx.x < outs * P; u += kCombineThreads) {
+        // lane u: chunk bits 0-1 from u's bits 0-1 and the rest from its bits
+        // above lg + 2, piece lane from the lg bits between, so that four
+        // lanes in a row read 64 contiguous bytes of one piece and the P
+        // lanes of a chunk sit 4 apart in the same wave.  Every lane takes
+        // part in the shuffles; lanes past the end redo the last chunk and
+        // store nothing.
+        const int o = ((u >> (lg + 2)) << 2) | (u & 3), p = (u >> 2) & (P - 1);
+        const int oc = min(o, outs - 1);
+        const int row = i + (oc / kChunks) * nb, c4 = oc % kChunks;
+        const int hi = row / G, hh = row - hi * G;
+        Lse r = {-INFINITY, 0.f, {0.f, 0.f, 0.f, 0.f}};
+        lse_pieces(a, r, first, n, p, P, hi, hh, c4);   // lane p < P <= n holds a piece
+        for (int x = 4; x < 4 * P; x <<= 1) {
+            const float m2 = __shfl_xor(r.m, x), l2 = __shfl_xor(r.l, x);
+            f32x4 o2;
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                o2[k] = __shfl_xor(r.o[k], x);
+            const float M = fmaxf(r.m, m2);
+            const float s1 = __builtin_amdgcn_exp2f(r.m - M), s2 = __builtin_amdgcn_exp2f(m2 - M);
+            r.l = r.l * s1 + l2 * s2;
+            r.o = r.o * s1 + o2 * s2;
+            r.m = M;
+        }
+        if (o < outs && p == 0)
+            store_out<MODE>(a, ((size_t)b * a.Hq + (q * a.HW + hi) * G + hh) * kHeadDim + 4 * c4,
+                            r.o * (1.0f / r.l));
+    }
+}
+
 template <int MODE>
 __global__ void __launch_bounds__(kCombineThreads)
 combine_kernel(const CombineArgs a)
 {
-    __shared__ float s_m[kCombineLanes][kHeadDim / 4];
-    __shared__ float s_l[kCombineLanes][kHeadDim / 4];
-    __shared__ f32x4 s_o[kCombineLanes][kHeadDim / 4];
+    // the first item's boundary record is requested with the header, not
+    // after it; entries past the plan's ranges (clamped into the array) are
+    // read but not used
+    const int last = a.cap - 1;
+    int4 rec = a.bounds[min((int)blockIdx.x + 1, last)];
     const int W = a.hdr->n_ranges, n_empty = a.hdr->n_empty;
-    const int G = a.G, HW = a.HW, Hg = a.Hkv / a.HW;
-    const int rows = HW * G;
+    // both loads in flight together: an empty use of all values here keeps
+    // the record's load from being moved past the branch on the header
+    asm volatile("" ::"s"(rec.x), "s"(rec.y), "s"(rec.z), "s"(rec.w), "s"(W), "s"(n_empty));
+    const int rows = a.HW * a.G, Hg = a.Hkv / a.HW;
     const int n_bounds = W > 1 ? W - 1 : 0;
     for (int item = blockIdx.x; item < n_bounds + n_empty; item += a.grid) {
+        // the next item's record is in flight while this one is merged
+        const int4 rec_next = a.bounds[min(item + a.grid + 1, last)];
         if (item >= n_bounds) {
             const int b = a.empty[item - n_bounds];
-            for (int u = threadIdx.x; u < a.Hq * (kHeadDim / 4); u += kCombineThreads)
+            for (int u = threadIdx.x; u < a.Hq * kChunks; u += kCombineThreads)
                 store_out<MODE>(a, (size_t)b * a.Hq * kHeadDim + 4 * u, f32x4{0.f, 0.f, 0.f, 0.f});
-            continue;
+        } else {
+            merge_boundary<MODE>(a, rec, rows, Hg);
         }
-        const int4 rec = a.bounds[item + 1];
-        const int s = rec.x, first = rec.y, n = rec.z, i = rec.w;
-        const int b = s / Hg, q = s - b * Hg;
-        if (n == 0 || (n <= kShortMerge && i != 0))
-            continue;
-        if (n <= kShortMerge) {
-            for (int u = threadIdx.x; u < rows * (kHeadDim / 4); u += kCombineThreads) {
-                const int row = u / (kHeadDim / 4), c4 = u - row * (kHeadDim / 4);
-                const int hi = row / G, hh = row - hi * G;
-                Lse r = {-INFINITY, 0.f, {0.f, 0.f, 0.f, 0.f}};
-                lse_pieces(a, r, first, n, 0, 1, hi, hh, c4);
-                store_out<MODE>(a, ((size_t)b * a.Hq + (q * HW + hi) * G + hh) * kHeadDim + 4 * c4,
-                                r.o * (1.0f / r.l));
-            }
-            continue;
-        }
-        for (int row = i; row < rows; row += n - 1) {
-            const int hi = row / G, hh = row - hi * G;
-            const int c4 = threadIdx.x & (kHeadDim / 4 - 1);
-            const int pl = threadIdx.x / (kHeadDim / 4);
-            Lse r = {-INFINITY, 0.f, {0.f, 0.f, 0.f, 0.f}};
-            lse_pieces(a, r, first, n, pl, kCombineLanes, hi, hh, c4);
-            s_m[pl][c4] = r.m;
-            s_l[pl][c4] = r.l;
-            s_o[pl][c4] = r.o;
-            __syncthreads();
-            if (pl == 0) {
-                // every lane holds at least one piece (n > kShortMerge >= lanes)
-                float Mt = -INFINITY;
-#pragma unroll
-                for (int x = 0; x < kCombineLanes; ++x)
-                    Mt = fmaxf(Mt, s_m[x][c4]);
-                float lt = 0.f;
-                f32x4 o = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int x = 0; x < kCombineLanes; ++x) {
-                    const float w = __builtin_amdgcn_exp2f(s_m[x][c4] - Mt);
-                    lt += w * s_l[x][c4];
-                    o += w * s_o[x][c4];
-                }
-                store_out<MODE>(a, ((size_t)b * a.Hq + (q * HW + hi) * G + hh) * kHeadDim + 4 * c4,
-                                o * (1.0f / lt));
-            }
-            __syncthreads();
-        }
+        rec = rec_next;
     }
 }
 
@@ -1490,6 +1496,7 @@ int enqueue_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, cons
     c.Hkv = n_kv_heads;
     c.G = n_q_heads / n_kv_heads;
     c.HW = heads_per_group(n_kv_heads);
+    c.cap = (int)lay.cap;
     int cus = 0;
     const int st = num_cus(&cus);
     if (st)

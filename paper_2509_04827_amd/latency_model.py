@@ -71,10 +71,12 @@ def fit_beta(f_mhz, t) -> float:
     return float(-b)
 
 
-def load_surface(path: str, n_q_heads: int | None = 32, column: str = "us_step"):
+def load_surface(path: str, n_q_heads: int | None = 32, column: str = "us_step_graph"):
     """Rows of a latency-surface CSV as (n_req, n_kv, step time) arrays;
-    `column` picks the eager step time (us_step) or the graph replay time
-    (us_step_graph)."""
+    `column` picks the device time per step (us_step_graph, steps replayed
+    from a HIP graph: what an engine that captures its decode iteration
+    sees) or the step time when each step is launched from Python
+    (us_step, which at small steps is the binding's call rate)."""
     with open(path) as f:
         rows = [r for r in csv.DictReader(f)
                 if n_q_heads is None or int(r["n_q_heads"]) == n_q_heads]

@@ -168,3 +168,40 @@ def test_binding_constants_match_header():
         assert getattr(vd, name) == int(val), name
     assert vd.VD_FLAG_RANGE_SHIFT == int(re.search(r"#define VD_FLAG_RANGE_SHIFT (\d+)u", hdr).group(1))
 
+
+
+def test_binding_rejects_host_and_strided_tensors_before_any_call():
+    """The binding's marshalling: host tensors, strided views and wrong dtypes
+    raise ValueError naming the problem; nothing reaches the library."""
+    import torch
+    t = torch.zeros(4, 8, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="device tensors"):
+        vd._ptr(t)
+    with pytest.raises(ValueError, match="contiguous"):
+        vd._ptr(t.t())
+    assert vd._ptr(None) is None
+    bf, i32, f32 = torch.bfloat16, torch.int32, torch.float32
+    ok = [torch.zeros(1, dtype=d) for d in (bf, bf, bf, i32, i32, bf)]
+    vd._attn_dtypes(*ok)
+    vd._attn_dtypes(*ok[:5], torch.zeros(1, dtype=f32))
+    for i, name in enumerate(("q", "k_pages", "v_pages", "page_table", "seq_lens", "out")):
+        bad = list(ok)
+        bad[i] = torch.zeros(1, dtype=torch.float16)
+        with pytest.raises(ValueError, match=name):
+            vd._attn_dtypes(*bad)
+    assert vd._stream(12345) == 12345          # raw hipStream_t handles pass through
+
+
+def test_binding_prototypes_match_the_header():
+    """Every export has a ctypes prototype with as many arguments as its C
+    declaration (pointers are passed as ints, which need the prototype to
+    travel as 64-bit pointers)."""
+    src = open(os.path.join(ROOT, "include", "vdecode.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    decl = dict(re.findall(r"\b(vd_[a-z_0-9]+)\s*\(([^)]*)\)\s*;", src))
+    L = vd.lib()
+    assert set(decl) == set(vd.EXPORTS)
+    for name, params in decl.items():
+        n = 0 if params.strip() in ("", "void") else params.count(",") + 1
+        assert getattr(L, name).argtypes is not None, name
+        assert len(getattr(L, name).argtypes) == n, (name, len(getattr(L, name).argtypes), n)
