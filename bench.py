@@ -224,6 +224,93 @@ def latency_surface(outdir: str, iters: int = 10, warmup: int = 3):
     print(json.dumps({"surface_points": len(rows), "fit": fit, "fit_graph": fit_graph}), flush=True)
 
 
+def cpu_configs(outdir: str, iters: int = 10):
+    """The oracle on the host cores against the GPU, for every seeded
+    workload: one wall-clock oracle run with all threads (and one with a
+    single thread for the tiny batch), beside the GPU's device time per step
+    (10 steps captured into one HIP graph, replayed 3 times after a
+    warm-up replay).  Writes oracle_cpu_baseline.{csv,json}."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2509_04827_amd as vd
+    from workloads import WORKLOADS, bits, kv_bytes, make_case
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    rows = []
+    for name in ("tiny_b4", "llama8b_b64", "chat_b256", "gqa8_b128", "long_b16"):
+        c = make_case(WORKLOADS[name], seed=0, fill="zero")
+        q, k, v = c["q"].to(dev), c["k_pages"].to(dev), c["v_pages"].to(dev)
+        pt, sl = c["page_table"].to(dev), c["seq_lens"].to(dev)
+        out = torch.empty(q.shape, dtype=torch.bfloat16, device=dev)
+        B, Hq, Hkv, maxp = c["num_seqs"], c["n_q_heads"], c["n_kv_heads"], c["max_pages_per_seq"]
+        ws = vd.alloc_workspace(B, Hq, Hkv, maxp)
+
+        def step():
+            vd.vd_decode_attn(q, k, v, pt, sl, out, c["scale"], ws)
+
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(iters):
+                step()
+        settle_clocks(graph.replay, 0.05)
+        graph.replay()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(3):
+            graph.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us_gpu = e0.elapsed_time(e1) * 1e3 / (3 * iters)
+        del graph
+
+        hq, hk, hv = bits(c["q"]), bits(c["k_pages"]), bits(c["v_pages"])
+        hpt, hsl = c["page_table"].numpy(), c["seq_lens"].numpy()
+        runs = [("all", 0)] + ([("single", 1)] if name == "tiny_b4" else [])
+        kvb = kv_bytes(c)
+        for tag, nthreads in runs:
+            t1 = time.time()
+            oracle.decode_attn(hq, hk, hv, hpt, hsl, c["scale"], nthreads=nthreads)
+            sec = time.time() - t1
+            rows.append(dict(workload=name, n_req=B, n_kv=c["n_kv"], kv_bytes=kvb,
+                             cpu_threads=oracle.max_threads() if nthreads == 0 else nthreads,
+                             cpu_s=round(sec, 4), cpu_kv_gbs=round(kvb / sec / 1e9, 3),
+                             gpu_us=round(us_gpu, 2), gpu_kv_gbs=round(kvb / us_gpu / 1e3, 1),
+                             gpu_over_cpu=round(sec * 1e6 / us_gpu, 1)))
+            print("cpu-configs %-12s threads %3d  cpu %8.3f s (%6.2f GB/s)  gpu %9.2f us (%7.1f GB/s)"
+                  % (name, rows[-1]["cpu_threads"], sec, kvb / sec / 1e9, us_gpu, kvb / us_gpu / 1e3),
+                  file=sys.stderr, flush=True)
+        del q, k, v, pt, sl, out, ws
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+    except OSError:
+        pass
+    os.makedirs(outdir, exist_ok=True)
+    keys = list(rows[0].keys())
+    with open(os.path.join(outdir, "oracle_cpu_baseline.csv"), "w") as f:
+        f.write(",".join(keys) + "\n")
+        for r in rows:
+            f.write(",".join(str(r[k]) for k in keys) + "\n")
+    info = {"cpu_model": cpu_model, "nproc": os.cpu_count(), "oracle_threads": oracle.max_threads(),
+            "rows": rows}
+    with open(os.path.join(outdir, "oracle_cpu_baseline.json"), "w") as f:
+        json.dump(info, f, indent=1)
+    print(json.dumps({"cpu_configs": len(rows), "cpu_model": cpu_model, "nproc": os.cpu_count()}),
+          flush=True)
+
+
 GEMM_SHAPES = (("qkv", 6144, 4096), ("o_proj", 4096, 4096), ("gate_up", 28672, 4096),
                ("down", 4096, 14336))
 GEMM_M = (1, 2, 4, 8, 16, 24, 32, 48, 64, 96, 128, 160, 192, 224, 240, 248, 255, 256, 257, 264,
@@ -414,6 +501,9 @@ def main():
     ap.add_argument("--clock-sweep", metavar="DIR", default=None,
                     help="instead of the bench line, time the attention kernel against the "
                          "shader clock it ran at and write DIR/decode_clock_sweep.{csv,json}")
+    ap.add_argument("--cpu-configs", metavar="DIR", default=None,
+                    help="time the oracle on the host cores and the GPU on every seeded workload; "
+                         "write oracle_cpu_baseline.{csv,json} to DIR")
     ap.add_argument("--surface", metavar="DIR", default=None,
                     help="instead of the bench line, measure the latency surface over "
                          "(batch, tokens per request) and write DIR/decode_latency_surface.{csv,md}")
@@ -440,6 +530,9 @@ def main():
         return
     if args.clock_sweep:
         clock_sweep(args.clock_sweep)
+        return
+    if args.cpu_configs:
+        cpu_configs(args.cpu_configs)
         return
 
     w = WORKLOADS[args.workload]
