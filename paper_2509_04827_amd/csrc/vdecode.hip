@@ -946,10 +946,13 @@ __device__ inline void attn_body(const AttnArgs &a)
         int n_res = 0;
         auto flush = [&]() {
             constexpr int kF32Chunks = G * kHeadDim / 4, kBf16Chunks = G * kHeadDim / 8;
+            static_assert(kDefer <= 64, "one entry's {whole, target} per lane");
+            // every entry's {whole, target} in one LDS read (lane e: entry e),
+            // so the loop below waits on LDS only for the entries' data
+            const int2 meta = s_meta[hi][min(lane, kDefer - 1)];
             for (int e = 0; e < n_res; ++e) {
-                const int2 m = s_meta[hi][e];
-                const int whole = __builtin_amdgcn_readfirstlane(m.x);
-                const int tgt = __builtin_amdgcn_readfirstlane(m.y);
+                const int whole = __builtin_amdgcn_readlane(meta.x, e);
+                const int tgt = __builtin_amdgcn_readlane(meta.y, e);
                 const float *st = s_res[hi][e];
                 if (whole && MODE == MODE_BF16) {
                     uint16_t *o = (uint16_t *)a.out + (size_t)tgt * kHeadDim;
