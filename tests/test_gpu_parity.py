@@ -582,6 +582,53 @@ def test_random_shapes(trial):
     check_bf16(run_gpu(d, torch.bfloat16, flags=flags), ref, "random %d" % trial)
 
 
+@pytest.mark.parametrize("trial", range(40))
+def test_random_sweep(trial):
+    """A wider seeded sweep: up to 400 requests, KV heads 1-16, every GQA
+    ratio, four length laws (short, lognormal, page boundaries, uniform) with
+    empty requests and an occasional 10k-60k-token request, table strides
+    past the longest request, and forced range lengths.  fp32 output against
+    the oracle; the staged calls (planner kernel) equal the whole step bit
+    for bit."""
+    rng = np.random.default_rng(9000 + trial)
+    hkv = int(rng.choice([1, 2, 4, 8, 16]))
+    G = int(rng.choice([1, 2, 4, 8, 16]))
+    G = min(G, max(1, 128 // hkv))
+    B = int(np.exp(rng.uniform(0, np.log(400))))
+    law = trial % 4
+    if law == 0:
+        lengths = rng.integers(0, 40, B)
+    elif law == 1:
+        lengths = np.clip(np.round(np.exp(rng.normal(np.log(300), 1.0, B))), 0, 20000)
+    elif law == 2:
+        lengths = rng.choice([0, 1, 15, 16, 17, 31, 32, 33, 63, 64, 65, 255, 256, 257, 1024], B)
+    else:
+        lengths = rng.integers(1, 3000, B)
+    lengths = [int(x) for x in lengths]
+    if rng.random() < 0.2:
+        lengths[int(rng.integers(0, B))] = int(rng.integers(10000, 60000))
+    stride = max(1, max((x + 15) // 16 for x in lengths)) + int(rng.integers(0, 4))
+    flags = vd.VD_FLAG_RANGE_TILES(int(rng.integers(1, 256))) if rng.random() < 0.3 else 0
+    what = "sweep %d B %d G %d Hkv %d flags %#x N_kv %d" % (trial, B, G, hkv, flags, sum(lengths))
+    say("case: " + what)
+    c = custom(lengths, hq=G * hkv, hkv=hkv, seed=9500 + trial, pt_stride=stride)
+    d = dev_case(c)
+    ref = ref_of(c)
+    whole = run_gpu(d, torch.float32, flags=flags)
+    check_f32(whole, ref, what)
+    if trial % 4 == 0:
+        check_bf16(run_gpu(d, torch.bfloat16, flags=flags), ref, what)
+    maxp = d["page_table"].shape[1]
+    ws = vd.alloc_workspace(B, G * hkv, hkv, maxp, flags)
+    staged = torch.full(d["q"].shape, float("nan"), dtype=torch.float32, device=DEV)
+    vd.vd_decode_plan(d["seq_lens"], G * hkv, hkv, maxp, ws, flags=flags)
+    vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"], staged,
+                         d["scale"], ws, flags=flags)
+    vd.vd_decode_combine(staged, hkv, maxp, ws, flags=flags)
+    torch.cuda.synchronize()
+    assert torch.equal(staged.view(torch.int32).cpu(), whole.view(torch.int32).cpu()), what
+
+
 # ------------------------------------------------------------------ KV append
 def test_kv_append_bit_exact():
     say("case: KV append")
