@@ -139,8 +139,8 @@ int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
 /*
  * Stage 1 of 3: lay every (page, KV head) tile of the step out in one sequence
  * (request, KV head, page order) and cut it into equal ranges, as many as
- * (or a multiple of) the attention workgroups the device runs at once (fewer
- * for small steps), so every wave streams the same number of tiles whatever
+ * (or a multiple of) the attention workgroups the device runs at once (one
+ * per tile when the step has fewer tiles), so every wave streams the same number of tiles whatever
  * the length mix; write that plan into the workspace.  Depends only
  * on seq_lens and the sizes, so one plan serves every layer of a decode step.
  * Not needed before a vd_decode_partial with VD_FLAG_SELF_PLAN, which cuts

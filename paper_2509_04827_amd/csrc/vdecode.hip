@@ -14,9 +14,11 @@
 // the step are laid out in one sequence, ordered by (request b, head group
 // q, page j); a "segment" is the run of tiles of one (b, q).  The plan
 // cuts the sequence into W ranges of equal length (W a multiple of the
-// number of resident workgroups: four waves per CU), so every workgroup
-// streams the same number of tiles whatever the length mix.  A range may end inside a segment and
-// may span several; each (range, segment) overlap is a "piece".  A piece that
+// number of resident workgroups, four waves per CU, or one range per tile
+// when there are fewer tiles than workgroups), so every workgroup streams
+// the same number of tiles whatever the length mix.  A range may end inside
+// a segment and may span several; each (range, segment) overlap is a
+// "piece".  A piece that
 // covers its whole segment writes the final output, the others write a (max,
 // normaliser, accumulator) partial per head that the combine kernel merges.
 // Pieces form a monotone path in (range, segment), so range + segment numbers
