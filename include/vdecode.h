@@ -42,6 +42,8 @@
  *   - Work is enqueued on `stream` and the call returns at once.
  *   - Argument errors are found on the host before anything is enqueued and
  *     return a nonzero vd_status; VD_ERROR_LAUNCH reports a failed launch.
+ *   - num_seqs = 0 is valid: the arguments are checked as usual, then the
+ *     call returns VD_SUCCESS with nothing enqueued.
  *   - Device-resident data is not validated: 0 <= L_b and every page id a
  *     request uses is a valid page of the pools are preconditions.  L_b larger
  *     than max_pages_per_seq * page_size is clamped to it.

@@ -205,3 +205,28 @@ def test_binding_prototypes_match_the_header():
         n = 0 if params.strip() in ("", "void") else params.count(",") + 1
         assert getattr(L, name).argtypes is not None, name
         assert len(getattr(L, name).argtypes) == n, (name, len(getattr(L, name).argtypes), n)
+
+
+def test_empty_batch_is_a_no_op():
+    """num_seqs = 0 with valid arguments returns VD_SUCCESS from every
+    per-request entry point without launching anything (so no device is
+    needed here); its arguments are still checked."""
+    L = vd.lib()
+    big = 1 << 30
+    ws = vd.vd_decode_workspace_size(0, 32, 8, 128, 16, 4, 0)
+    assert ws > 0
+    attn = (FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 32, 8, 128, 16, 0.125, 4, FAKE, big, 0, None)
+    assert L.vd_decode_attn(*attn) == vd.VD_SUCCESS
+    assert L.vd_decode_partial(*attn) == vd.VD_SUCCESS
+    assert L.vd_decode_plan(FAKE, 0, 32, 8, 128, 16, 4, FAKE, big, 0, None) == vd.VD_SUCCESS
+    assert L.vd_decode_combine(FAKE, 0, 32, 8, 128, 16, 4, FAKE, big, 0, None) == vd.VD_SUCCESS
+    assert L.vd_decode_gather(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 8, 128, 16, 4, FAKE, big,
+                              None) == vd.VD_SUCCESS
+    assert L.vd_kv_append(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 8, 128, 16, 4, None) == vd.VD_SUCCESS
+    # still validated: a NULL output or a short workspace is an error
+    bad = list(attn)
+    bad[5] = None
+    assert L.vd_decode_attn(*bad) == vd.VD_ERROR_INVALID_VALUE
+    bad = list(attn)
+    bad[14] = 16
+    assert L.vd_decode_attn(*bad) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
