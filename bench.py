@@ -477,6 +477,73 @@ def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
     print(json.dumps({"gemm_points": len(rows)}), flush=True)
 
 
+def next_profile(outdir: str, iters: int = 20, warmup: int = 3):
+    """A short, profiler-friendly run of the other kernels: vd_gemm_bf16 on
+    the four Llama-3-8B-shaped projections at M = 1, 16 and 64, then
+    vd_kv_append on the chat batch's sizes (256 requests, 8 KV heads).  Each
+    case is a burst of `iters` calls after `warmup` calls, with a 5 ms pause
+    before it, so a kernel trace splits into one burst per case in the order
+    of next_profile.csv, and starts with one vd_stream_read of 4 KiB (a
+    marker dispatch, so counter runs without timestamps split by case too).
+    Optionally ends with --copy-calibration copies."""
+    import numpy as np
+    import torch
+
+    import paper_2509_04827_amd as vd
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    gen = torch.Generator(device=dev).manual_seed(0)
+    stream = torch.cuda.current_stream()
+    rows = []
+    marker = torch.zeros(4096, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+
+    def burst(fn):
+        vd.vd_stream_read(marker, sink, blocks=1, stream=stream)
+        settle_clocks(fn, 0.02)
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        time.sleep(0.005)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(iters):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        time.sleep(0.005)
+        return e0.elapsed_time(e1) * 1e3 / iters
+
+    for name, N, K in GEMM_SHAPES:
+        w = torch.randn((N, K), generator=gen, device=dev).to(torch.bfloat16)
+        for M in (1, 16, 64):
+            x = torch.randn((M, K), generator=gen, device=dev).to(torch.bfloat16)
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            ws = torch.empty(max(16, vd.vd_gemm_workspace_size(M, N, K)), dtype=torch.uint8, device=dev)
+            us = burst(lambda: vd.vd_gemm_bf16(x, w, y, ws, stream=stream))
+            rows.append(dict(case="gemm_%s_M%d" % (name, M), calls=iters, us_events=round(us, 2),
+                             algorithmic_bytes=(N * K + M * K + M * N) * 2))
+        del w
+    B, Hkv, S, maxp = 256, 8, 16, 4
+    pages = torch.randperm(B * maxp, generator=torch.Generator().manual_seed(1)).to(torch.int32)
+    pt = pages.view(B, maxp).to(dev)
+    kp = torch.zeros((B * maxp, S, Hkv, 128), dtype=torch.bfloat16, device=dev)
+    vp = torch.zeros_like(kp)
+    kn = torch.randn((B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
+    vn = torch.randn((B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
+    pos = torch.arange(B, dtype=torch.int32, device=dev) % (maxp * S)
+    us = burst(lambda: vd.vd_kv_append(kn, vn, kp, vp, pt, pos, stream=stream))
+    rows.append(dict(case="kv_append_B256", calls=iters, us_events=round(us, 2),
+                     algorithmic_bytes=2 * 2 * B * Hkv * 128 * 2 + B * 8))
+    os.makedirs(outdir, exist_ok=True)
+    with open(os.path.join(outdir, "next_profile.csv"), "w") as f:
+        f.write("case,calls,us_events,algorithmic_bytes\n")
+        for r in rows:
+            f.write("%s,%d,%.2f,%d\n" % (r["case"], r["calls"], r["us_events"], r["algorithmic_bytes"]))
+    print(json.dumps({"next_profile_cases": len(rows)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -501,6 +568,9 @@ def main():
     ap.add_argument("--clock-sweep", metavar="DIR", default=None,
                     help="instead of the bench line, time the attention kernel against the "
                          "shader clock it ran at and write DIR/decode_clock_sweep.{csv,json}")
+    ap.add_argument("--next-profile", metavar="DIR", default=None,
+                    help="short run of the GEMM (4 shapes x M 1/16/64) and KV-append kernels "
+                         "for a kernel trace; writes next_profile.csv to DIR")
     ap.add_argument("--cpu-configs", metavar="DIR", default=None,
                     help="time the oracle on the host cores and the GPU on every seeded workload; "
                          "write oracle_cpu_baseline.{csv,json} to DIR")
@@ -533,6 +603,16 @@ def main():
         return
     if args.cpu_configs:
         cpu_configs(args.cpu_configs)
+        return
+    if args.next_profile:
+        next_profile(args.next_profile)
+        if args.copy_calibration:
+            n = args.copy_calibration // 4
+            src = torch.ones(n, dtype=torch.int32, device="cuda:0")
+            dst = torch.empty_like(src)
+            for _ in range(3):
+                dst.copy_(src)
+            torch.cuda.synchronize()
         return
 
     w = WORKLOADS[args.workload]
