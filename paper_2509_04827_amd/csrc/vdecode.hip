@@ -1077,11 +1077,11 @@ struct CombineArgs {
 // and its own index i among the segment's n - 1 inner boundaries.  Boundary
 // i merges query-head rows i, i + n - 1, ... of the segment's HW * G rows,
 // so the rows are spread over the workgroups of all its boundaries.  Each
-// output chunk (row, 4 floats of head_dim) gets P adjacent lanes, P a power
-// of two no larger than n or kCombineMaxLanes, as many as the threads allow;
-// lane p merges pieces p, p + P, ... (the loads of four pieces issued
+// output chunk (row, 4 floats of head_dim) gets P lanes of one wave, P a
+// power of two no larger than n or kCombineMaxLanes, as many as the threads
+// allow; lane p merges pieces p, p + P, ... (the loads of four pieces issued
 // before use), then the P lanes' (max, normaliser, accumulator) are merged
-// by lane shuffles within the wave.  A small step's merge is then one round of loads.
+// by lane shuffles.  A small step's merge is then one round of loads.
 // Merging is a running log-sum-exp in the exp2 domain.
 constexpr int kChunks = kHeadDim / 4;     // float4 chunks of one query head's output
 constexpr int kCombineMaxLanes = 16;
