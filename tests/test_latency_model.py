@@ -1,4 +1,5 @@
-"""Decode latency model (Eq. pred-itl fit and boosted trees) on synthetic data."""
+"""Decode latency model (Eq. pred-itl fit and boosted trees) on synthetic data,
+and on the latency surface measured on the GPU (profiles/)."""
 import numpy as np
 
 from paper_2509_04827_amd import latency_model as lm
@@ -67,3 +68,19 @@ def test_clock_scaled_fit():
     slow = m.at(1200.0)
     assert abs(slow.d / base.d - 2.0 ** 0.095) < 1e-12 and abs(slow.e / base.e - 2.0 ** 0.095) < 1e-12
 
+
+def test_committed_surface_loads_and_fits():
+    """The measured surface under profiles/ parses with both time columns
+    (device time from graph replays, and Python-launched steps), and the
+    decode model fits it: R^2 near 1 and a per-token cost d that implies a
+    KV read rate below the 8 TB/s of HBM and above half of it."""
+    import os
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "profiles", "decode_latency_surface.csv")
+    for column in ("us_step_graph", "us_step"):
+        n_req, n_kv, t = lm.load_surface(path, column=column)
+        assert len(t) >= 100 and (t > 0).all()
+        f = lm.fit_linear(n_req, n_kv, t)
+        assert f.r2 > 0.999
+        assert 4000 < f.kv_bandwidth_gbs() < 8000
+        assert 0 < f.e < 50
