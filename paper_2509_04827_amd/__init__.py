@@ -158,10 +158,18 @@ def step_info(workspace) -> dict:
             "first_group_us": dt * 0.01, "sclk_mhz": (c1 - c0) * 100.0 / dt}
 
 
-def _stream(stream):
-    """hipStream_t of `stream`: torch's current stream when None, a
-    torch.cuda.Stream, or a raw handle (int) taken from one."""
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
+def _stream(stream, t=None):
+    """hipStream_t of `stream`: torch's current stream (on t's device) when
+    None, a torch.cuda.Stream, or a raw handle (int) taken from one.  The
+    current stream's handle is read without building a Stream object when
+    torch offers that (a few microseconds less per call)."""
     if stream is None:
+        dev = -1 if t is None else t.get_device()
+        if _raw_stream is not None and dev >= 0:
+            return _raw_stream(dev)
         return torch.cuda.current_stream().cuda_stream
     if isinstance(stream, int):
         return stream
@@ -190,14 +198,14 @@ def vd_decode_attn(q, k_pages, v_pages, page_table, seq_lens, out, scale: float,
     _check(lib().vd_decode_attn(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(page_table),
                                 _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale), maxp,
                                 _ptr(workspace), workspace.numel(), _out_flags(out, flags),
-                                _stream(stream)), "vd_decode_attn")
+                                _stream(stream, out)), "vd_decode_attn")
 
 
 def vd_decode_plan(seq_lens, n_q_heads: int, n_kv_heads: int, max_pages_per_seq: int, workspace,
                    flags: int = 0, head_dim: int = 128, page_size: int = 16, stream=None) -> None:
     _check(lib().vd_decode_plan(_ptr(seq_lens), seq_lens.shape[0], n_q_heads, n_kv_heads,
                                 head_dim, page_size, max_pages_per_seq, _ptr(workspace),
-                                workspace.numel(), flags, _stream(stream)), "vd_decode_plan")
+                                workspace.numel(), flags, _stream(stream, seq_lens)), "vd_decode_plan")
 
 
 def vd_decode_partial(q, k_pages, v_pages, page_table, seq_lens, out, scale: float, workspace,
@@ -207,7 +215,7 @@ def vd_decode_partial(q, k_pages, v_pages, page_table, seq_lens, out, scale: flo
     _check(lib().vd_decode_partial(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(page_table),
                                    _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale),
                                    maxp, _ptr(workspace), workspace.numel(),
-                                   _out_flags(out, flags), _stream(stream)), "vd_decode_partial")
+                                   _out_flags(out, flags), _stream(stream, out)), "vd_decode_partial")
 
 
 def vd_decode_combine(out, n_kv_heads: int, max_pages_per_seq: int, workspace, flags: int = 0,
@@ -215,7 +223,7 @@ def vd_decode_combine(out, n_kv_heads: int, max_pages_per_seq: int, workspace, f
     B, Hq, D = out.shape
     _check(lib().vd_decode_combine(_ptr(out), B, Hq, n_kv_heads, D, page_size, max_pages_per_seq,
                                    _ptr(workspace), workspace.numel(), _out_flags(out, flags),
-                                   _stream(stream)), "vd_decode_combine")
+                                   _stream(stream, out)), "vd_decode_combine")
 
 
 def vd_decode_gather(k_pages, v_pages, page_table, seq_lens, k_out, v_out, workspace,
@@ -224,7 +232,7 @@ def vd_decode_gather(k_pages, v_pages, page_table, seq_lens, k_out, v_out, works
     _check(lib().vd_decode_gather(_ptr(k_pages), _ptr(v_pages), _ptr(page_table), _ptr(seq_lens),
                                   _ptr(k_out), _ptr(v_out), seq_lens.shape[0], Hkv, D, S,
                                   page_table.shape[1], _ptr(workspace), workspace.numel(),
-                                  _stream(stream)), "vd_decode_gather")
+                                  _stream(stream, k_pages)), "vd_decode_gather")
 
 
 def vd_kv_append(k_new, v_new, k_pages, v_pages, page_table, positions, stream=None) -> None:
@@ -232,7 +240,7 @@ def vd_kv_append(k_new, v_new, k_pages, v_pages, page_table, positions, stream=N
     _, S, Hkv, D = k_pages.shape
     _check(lib().vd_kv_append(_ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages),
                               _ptr(page_table), _ptr(positions), positions.shape[0], Hkv, D, S,
-                              page_table.shape[1], _stream(stream)), "vd_kv_append")
+                              page_table.shape[1], _stream(stream, k_pages)), "vd_kv_append")
 
 
 def vd_gemm_workspace_size(M: int, N: int, K: int, flags: int = 0) -> int:
@@ -245,10 +253,10 @@ def vd_gemm_bf16(x, w, y, workspace=None, flags: int = 0, stream=None) -> None:
     N = w.shape[0]
     _check(lib().vd_gemm_bf16(_ptr(x), _ptr(w), _ptr(y), M, N, K, _ptr(workspace),
                               0 if workspace is None else workspace.numel(),
-                              _out_flags(y, flags), _stream(stream)), "vd_gemm_bf16")
+                              _out_flags(y, flags), _stream(stream, y)), "vd_gemm_bf16")
 
 
 def vd_stream_read(buf, sink, blocks: int = 16384, stream=None) -> None:
     """Read all of `buf` (a measurement of the HBM read rate; see the header)."""
     _check(lib().vd_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), int(blocks),
-                                _stream(stream)), "vd_stream_read")
+                                _stream(stream, buf)), "vd_stream_read")
