@@ -497,6 +497,53 @@ def test_staged_equals_whole_random(trial):
     assert torch.isfinite(whole).all()
 
 
+def test_hip_graph_replay_staged_layers():
+    """A decode iteration of a two-layer model in the staged form, captured
+    into one HIP graph: one plan, then attention and combine per layer (each
+    layer its own Q and KV pools, one workspace).  Every replay, with eager
+    work and a synchronisation between replays, equals the eager calls bit
+    for bit, and the per-layer outputs match the oracle."""
+    say("case: HIP graph capture and replay of plan + 2 x (partial, combine)")
+    layers = [custom([37, 700, 4100, 1, 0, 260], seed=21 + i) for i in range(2)]
+    ds = [dev_case(c) for c in layers]
+    maxp = layers[0]["max_pages_per_seq"]
+    assert all(c["max_pages_per_seq"] == maxp for c in layers)
+    assert all(torch.equal(c["seq_lens"], layers[0]["seq_lens"]) for c in layers)
+    B = layers[0]["num_seqs"]
+    ws = vd.alloc_workspace(B, 32, 8, maxp)
+
+    def iteration(outs):
+        vd.vd_decode_plan(ds[0]["seq_lens"], 32, 8, maxp, ws)
+        for d, o in zip(ds, outs):
+            vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
+                                 o, d["scale"], ws)
+            vd.vd_decode_combine(o, 8, maxp, ws)
+
+    eager = [torch.empty(d["q"].shape, dtype=torch.float32, device=DEV) for d in ds]
+    iteration(eager)
+    outs = [torch.empty_like(e) for e in eager]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        iteration(outs)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        iteration(outs)
+    for i in range(3):
+        for o in outs:
+            o.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        for o, e in zip(outs, eager):
+            assert torch.equal(o.view(torch.int32), e.view(torch.int32)), "replay %d" % i
+        iteration(eager)   # eager work between replays
+        torch.cuda.synchronize()
+    for o, c in zip(outs, layers):
+        check_f32(o, ref_of(c), "staged graph layer")
+
+
 def test_workspace_reuse_across_steps():
     """One workspace serves steps of different length mixes in a row: what a
     longer step left in it (ranges, boundary records, partials) never leaks
