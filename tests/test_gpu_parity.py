@@ -544,6 +544,31 @@ def test_hip_graph_replay_staged_layers():
         check_f32(o, ref_of(c), "staged graph layer")
 
 
+def test_concurrent_streams_distinct_workspaces():
+    """Two steps of different shapes enqueued on two streams at once, each
+    with its own workspace (default stream priorities): both results equal
+    the same steps run one after the other, bit for bit."""
+    say("case: two streams, two workspaces")
+    cases = [custom([3000, 17, 900, 0, 64], seed=25),
+             custom([5, 12000, 1, 300], hq=64, hkv=8, seed=26)]
+    ds = [dev_case(c) for c in cases]
+    wss = [vd.alloc_workspace(c["num_seqs"], c["n_q_heads"], c["n_kv_heads"], c["max_pages_per_seq"])
+           for c in cases]
+    serial = [run_gpu(d) for d in ds]
+    outs = [torch.full(d["q"].shape, float("nan"), dtype=torch.float32, device=DEV) for d in ds]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for d, o, ws, st in zip(ds, outs, wss, streams):
+            with torch.cuda.stream(st):
+                vd.vd_decode_attn(d["q"], d["k_pages"], d["v_pages"], d["page_table"],
+                                  d["seq_lens"], o, d["scale"], ws)
+    torch.cuda.synchronize()
+    for o, e, c in zip(outs, serial, cases):
+        assert torch.equal(o.view(torch.int32), e.view(torch.int32))
+        check_f32(o, ref_of(c), "concurrent")
+
+
 def test_workspace_reuse_across_steps():
     """One workspace serves steps of different length mixes in a row: what a
     longer step left in it (ranges, boundary records, partials) never leaks
