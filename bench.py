@@ -581,7 +581,7 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build measures one GPU; the decode-attention path has no "
+        print("bench.py measures one GPU: the decode-attention path has no "
               "multi-GPU mode (sequences shard across GPUs with no exchange). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
