@@ -113,11 +113,14 @@ typedef struct vd_step_info {
 /*
  * Bytes of device workspace a call with these sizes needs: the plan and the
  * split-K partials (per partial and query head: running max, normaliser and
- * an fp32 head_dim accumulator).  Independent of the actual lengths; grows
- * with num_seqs * max_pages_per_seq * n_kv_heads / 256 for very large caches.
+ * an fp32 head_dim accumulator).  Independent of the actual lengths and of
+ * the device; grows with num_seqs * max_pages_per_seq * n_kv_heads / 256 for
+ * very large caches.
  * `flags` as passed to the attention call: a forced range length
- * (VD_FLAG_RANGE_TILES) can need more room than the automatic plan.  Returns
- * 0 when the sizes or flags are invalid or unsupported.
+ * (VD_FLAG_RANGE_TILES) can need more room than the automatic plan.  (A size
+ * query over the attention sizes alone could not say so; this one takes the
+ * call's flags too.)  Returns 0 when the sizes or flags are invalid or
+ * unsupported.
  */
 size_t vd_decode_workspace_size(int num_seqs, int n_q_heads, int n_kv_heads,
                                 int head_dim, int page_size,
@@ -188,7 +191,9 @@ int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads,
  * matrix-operand assembly, and writes every cached K and V row it assembled
  * to k_out / v_out (bf16 [sum_b L_b][n_kv_heads][head_dim], requests in order,
  * tokens in logical order) instead of computing attention.  The result must
- * equal a host gather through page_table bit for bit.  Workspace as for
+ * equal a host gather through page_table bit for bit.  Unlike a plain copy
+ * it takes a workspace: the planner kernel writes the plan there and the
+ * kernel walks it as the attention kernel does.  Workspace as for
  * vd_decode_attn with n_q_heads = n_kv_heads.
  */
 int vd_decode_gather(const void *k_pages, const void *v_pages,

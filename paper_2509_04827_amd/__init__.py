@@ -181,9 +181,37 @@ def _check(st, where):
         raise VdError(st, where)
 
 
-def _attn_sizes(q, k_pages, page_table):
+def _shape(t, shape, what):
+    """Raise ValueError unless tensor t has exactly `shape` (None matches any
+    extent).  A mismatched tensor would otherwise be read or written out of
+    bounds on the device."""
+    if t.dim() != len(shape) or any(s is not None and t.shape[i] != s for i, s in enumerate(shape)):
+        want = "[%s]" % ", ".join("*" if s is None else str(s) for s in shape)
+        raise ValueError("%s has shape %s, expected %s" % (what, list(t.shape), want))
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def _kv_sizes(k_pages, v_pages):
+    _shape(k_pages, (None, None, None, None), "k_pages")
+    _shape(v_pages, tuple(k_pages.shape), "v_pages")
+    _, S, Hkv, D = k_pages.shape
+    return S, Hkv, D
+
+
+def _attn_sizes(q, k_pages, v_pages, page_table, seq_lens, out):
+    """Sizes of an attention call, read from q, k_pages and page_table; every
+    other tensor must agree with them."""
+    _shape(q, (None, None, None), "q")
     B, Hq, D = q.shape
-    _, S, Hkv, _ = k_pages.shape
+    S, Hkv, Dk = _kv_sizes(k_pages, v_pages)
+    if Dk != D:
+        raise ValueError("k_pages head_dim %d differs from q's %d" % (Dk, D))
+    _shape(page_table, (B, None), "page_table")
+    _shape(seq_lens, (B,), "seq_lens")
+    _shape(out, (B, Hq, D), "out")
     return B, Hq, Hkv, D, S, page_table.shape[1]
 
 
@@ -194,52 +222,79 @@ def _out_flags(out, flags):
 def vd_decode_attn(q, k_pages, v_pages, page_table, seq_lens, out, scale: float, workspace,
                    flags: int = 0, stream=None) -> None:
     _attn_dtypes(q, k_pages, v_pages, page_table, seq_lens, out)
-    B, Hq, Hkv, D, S, maxp = _attn_sizes(q, k_pages, page_table)
+    B, Hq, Hkv, D, S, maxp = _attn_sizes(q, k_pages, v_pages, page_table, seq_lens, out)
     _check(lib().vd_decode_attn(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(page_table),
                                 _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale), maxp,
-                                _ptr(workspace), workspace.numel(), _out_flags(out, flags),
+                                _ptr(workspace), _nbytes(workspace), _out_flags(out, flags),
                                 _stream(stream, out)), "vd_decode_attn")
 
 
 def vd_decode_plan(seq_lens, n_q_heads: int, n_kv_heads: int, max_pages_per_seq: int, workspace,
                    flags: int = 0, head_dim: int = 128, page_size: int = 16, stream=None) -> None:
+    _shape(seq_lens, (None,), "seq_lens")
     _check(lib().vd_decode_plan(_ptr(seq_lens), seq_lens.shape[0], n_q_heads, n_kv_heads,
                                 head_dim, page_size, max_pages_per_seq, _ptr(workspace),
-                                workspace.numel(), flags, _stream(stream, seq_lens)), "vd_decode_plan")
+                                _nbytes(workspace), flags, _stream(stream, seq_lens)), "vd_decode_plan")
 
 
 def vd_decode_partial(q, k_pages, v_pages, page_table, seq_lens, out, scale: float, workspace,
                       flags: int = 0, stream=None) -> None:
     _attn_dtypes(q, k_pages, v_pages, page_table, seq_lens, out)
-    B, Hq, Hkv, D, S, maxp = _attn_sizes(q, k_pages, page_table)
+    B, Hq, Hkv, D, S, maxp = _attn_sizes(q, k_pages, v_pages, page_table, seq_lens, out)
     _check(lib().vd_decode_partial(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(page_table),
                                    _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale),
-                                   maxp, _ptr(workspace), workspace.numel(),
+                                   maxp, _ptr(workspace), _nbytes(workspace),
                                    _out_flags(out, flags), _stream(stream, out)), "vd_decode_partial")
 
 
 def vd_decode_combine(out, n_kv_heads: int, max_pages_per_seq: int, workspace, flags: int = 0,
                       page_size: int = 16, stream=None) -> None:
+    _dtype(out, (_BF16, _F32), "out")
+    _shape(out, (None, None, None), "out")
     B, Hq, D = out.shape
     _check(lib().vd_decode_combine(_ptr(out), B, Hq, n_kv_heads, D, page_size, max_pages_per_seq,
-                                   _ptr(workspace), workspace.numel(), _out_flags(out, flags),
+                                   _ptr(workspace), _nbytes(workspace), _out_flags(out, flags),
                                    _stream(stream, out)), "vd_decode_combine")
 
 
 def vd_decode_gather(k_pages, v_pages, page_table, seq_lens, k_out, v_out, workspace,
                      stream=None) -> None:
-    _, S, Hkv, D = k_pages.shape
+    for t, n in ((k_pages, "k_pages"), (v_pages, "v_pages"), (k_out, "k_out"), (v_out, "v_out")):
+        _dtype(t, (_BF16,), n)
+    _dtype(page_table, (_I32,), "page_table")
+    _dtype(seq_lens, (_I32,), "seq_lens")
+    S, Hkv, D = _kv_sizes(k_pages, v_pages)
+    _shape(seq_lens, (None,), "seq_lens")
+    B = seq_lens.shape[0]
+    _shape(page_table, (B, None), "page_table")
+    # the output holds every gathered row: sum of the lengths as the kernels
+    # clamp them (a device read, so this call synchronises; it is a check)
+    maxp = page_table.shape[1]
+    rows = int(seq_lens.clamp(0, maxp * S).sum().item()) if B else 0
+    _shape(k_out, (None, Hkv, D), "k_out")
+    _shape(v_out, tuple(k_out.shape), "v_out")
+    if k_out.shape[0] < rows:
+        raise ValueError("k_out / v_out hold %d rows, the lengths need %d" % (k_out.shape[0], rows))
     _check(lib().vd_decode_gather(_ptr(k_pages), _ptr(v_pages), _ptr(page_table), _ptr(seq_lens),
-                                  _ptr(k_out), _ptr(v_out), seq_lens.shape[0], Hkv, D, S,
-                                  page_table.shape[1], _ptr(workspace), workspace.numel(),
+                                  _ptr(k_out), _ptr(v_out), B, Hkv, D, S,
+                                  maxp, _ptr(workspace), _nbytes(workspace),
                                   _stream(stream, k_pages)), "vd_decode_gather")
 
 
 def vd_kv_append(k_new, v_new, k_pages, v_pages, page_table, positions, stream=None) -> None:
     """Write k_new[b] / v_new[b] at token positions[b] of request b's pages."""
-    _, S, Hkv, D = k_pages.shape
+    for t, n in ((k_new, "k_new"), (v_new, "v_new"), (k_pages, "k_pages"), (v_pages, "v_pages")):
+        _dtype(t, (_BF16,), n)
+    _dtype(page_table, (_I32,), "page_table")
+    _dtype(positions, (_I32,), "positions")
+    S, Hkv, D = _kv_sizes(k_pages, v_pages)
+    _shape(positions, (None,), "positions")
+    B = positions.shape[0]
+    _shape(k_new, (B, Hkv, D), "k_new")
+    _shape(v_new, (B, Hkv, D), "v_new")
+    _shape(page_table, (B, None), "page_table")
     _check(lib().vd_kv_append(_ptr(k_new), _ptr(v_new), _ptr(k_pages), _ptr(v_pages),
-                              _ptr(page_table), _ptr(positions), positions.shape[0], Hkv, D, S,
+                              _ptr(page_table), _ptr(positions), B, Hkv, D, S,
                               page_table.shape[1], _stream(stream, k_pages)), "vd_kv_append")
 
 
@@ -249,14 +304,20 @@ def vd_gemm_workspace_size(M: int, N: int, K: int, flags: int = 0) -> int:
 
 def vd_gemm_bf16(x, w, y, workspace=None, flags: int = 0, stream=None) -> None:
     """y [M][N] = x [M][K] . w [N][K]^T (y fp32 sets VD_FLAG_OUT_F32)."""
+    _dtype(x, (_BF16,), "x")
+    _dtype(w, (_BF16,), "w")
+    _dtype(y, (_BF16, _F32), "y")
+    _shape(x, (None, None), "x")
     M, K = x.shape
+    _shape(w, (None, K), "w")
     N = w.shape[0]
+    _shape(y, (M, N), "y")
     _check(lib().vd_gemm_bf16(_ptr(x), _ptr(w), _ptr(y), M, N, K, _ptr(workspace),
-                              0 if workspace is None else workspace.numel(),
+                              0 if workspace is None else _nbytes(workspace),
                               _out_flags(y, flags), _stream(stream, y)), "vd_gemm_bf16")
 
 
 def vd_stream_read(buf, sink, blocks: int = 16384, stream=None) -> None:
     """Read all of `buf` (a measurement of the HBM read rate; see the header)."""
-    _check(lib().vd_stream_read(_ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), int(blocks),
+    _check(lib().vd_stream_read(_ptr(buf), _nbytes(buf), _ptr(sink), int(blocks),
                                 _stream(stream, buf)), "vd_stream_read")

@@ -230,3 +230,81 @@ def test_empty_batch_is_a_no_op():
     bad = list(attn)
     bad[14] = 16
     assert L.vd_decode_attn(*bad) == vd.VD_ERROR_WORKSPACE_TOO_SMALL
+
+
+def test_binding_rejects_mismatched_shapes_before_any_call():
+    """Sizes come from q, k_pages and page_table (attention), positions
+    (append) and x / w (GEMM); every other tensor must agree with them, or the
+    binding raises ValueError naming it before anything reaches the library
+    (a mismatched tensor would be read or written out of bounds)."""
+    import torch
+    bf, i32, f32 = torch.bfloat16, torch.int32, torch.float32
+    B, Hq, Hkv, D, S, maxp, P = 3, 8, 2, 128, 16, 4, 12
+
+    def attn_args(**kw):
+        a = dict(q=torch.zeros(B, Hq, D, dtype=bf), k=torch.zeros(P, S, Hkv, D, dtype=bf),
+                 v=torch.zeros(P, S, Hkv, D, dtype=bf), pt=torch.zeros(B, maxp, dtype=i32),
+                 sl=torch.zeros(B, dtype=i32), out=torch.zeros(B, Hq, D, dtype=f32))
+        a.update(kw)
+        return a
+
+    bad = {
+        "out": dict(out=torch.zeros(B, Hq, D + 1, dtype=f32)),
+        "v_pages": dict(v=torch.zeros(P - 1, S, Hkv, D, dtype=bf)),
+        "seq_lens": dict(sl=torch.zeros(B + 1, dtype=i32)),
+        "page_table": dict(pt=torch.zeros(B - 1, maxp, dtype=i32)),
+        "q": dict(q=torch.zeros(B, Hq * D, dtype=bf)),
+        "head_dim": dict(k=torch.zeros(P, S, Hkv, 64, dtype=bf), v=torch.zeros(P, S, Hkv, 64, dtype=bf)),
+    }
+    for entry in (vd.vd_decode_attn, vd.vd_decode_partial):
+        for what, kw in bad.items():
+            a = attn_args(**kw)
+            with pytest.raises(ValueError, match=what):
+                entry(a["q"], a["k"], a["v"], a["pt"], a["sl"], a["out"], 0.125, torch.zeros(16, dtype=torch.uint8))
+    # the well-shaped call gets past the shape checks and stops at the host tensors
+    a = attn_args()
+    with pytest.raises(ValueError, match="device tensors"):
+        vd.vd_decode_attn(a["q"], a["k"], a["v"], a["pt"], a["sl"], a["out"], 0.125,
+                          torch.zeros(16, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="out"):
+        vd.vd_decode_combine(torch.zeros(B, Hq * D, dtype=f32), Hkv, maxp, torch.zeros(16, dtype=torch.uint8))
+
+    k, v = torch.zeros(P, S, Hkv, D, dtype=bf), torch.zeros(P, S, Hkv, D, dtype=bf)
+    pt, sl = torch.zeros(B, maxp, dtype=i32), torch.full((B,), 20, dtype=i32)
+    ws = torch.zeros(16, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="k_out"):      # 60 rows needed
+        vd.vd_decode_gather(k, v, pt, sl, torch.zeros(59, Hkv, D, dtype=bf),
+                            torch.zeros(59, Hkv, D, dtype=bf), ws)
+    with pytest.raises(ValueError, match="v_out"):
+        vd.vd_decode_gather(k, v, pt, sl, torch.zeros(60, Hkv, D, dtype=bf),
+                            torch.zeros(60, Hkv + 1, D, dtype=bf), ws)
+    with pytest.raises(ValueError, match="page_table"):
+        vd.vd_decode_gather(k, v, pt[:2].contiguous(), sl, torch.zeros(60, Hkv, D, dtype=bf),
+                            torch.zeros(60, Hkv, D, dtype=bf), ws)
+
+    kn, vn, pos = torch.zeros(B, Hkv, D, dtype=bf), torch.zeros(B, Hkv, D, dtype=bf), torch.zeros(B, dtype=i32)
+    with pytest.raises(ValueError, match="k_new"):
+        vd.vd_kv_append(kn[:2].contiguous(), vn, k, v, pt, pos)
+    with pytest.raises(ValueError, match="v_new"):
+        vd.vd_kv_append(kn, torch.zeros(B, Hkv, D + 8, dtype=bf), k, v, pt, pos)
+    with pytest.raises(ValueError, match="page_table"):
+        vd.vd_kv_append(kn, vn, k, v, torch.zeros(B + 1, maxp, dtype=i32), pos)
+    with pytest.raises(ValueError, match="v_pages"):
+        vd.vd_kv_append(kn, vn, k, torch.zeros(P, S, Hkv, 64, dtype=bf), pt, pos)
+
+    x, w = torch.zeros(4, 512, dtype=bf), torch.zeros(64, 512, dtype=bf)
+    with pytest.raises(ValueError, match="w has shape"):
+        vd.vd_gemm_bf16(x, torch.zeros(64, 1024, dtype=bf), torch.zeros(4, 64, dtype=f32))
+    with pytest.raises(ValueError, match="y has shape"):
+        vd.vd_gemm_bf16(x, w, torch.zeros(4, 128, dtype=f32))
+    with pytest.raises(ValueError, match="y has shape"):
+        vd.vd_gemm_bf16(x, w, torch.zeros(5, 64, dtype=f32))
+    with pytest.raises(ValueError, match="x must be"):
+        vd.vd_gemm_bf16(x.float(), w, torch.zeros(4, 64, dtype=f32))
+
+
+def test_binding_passes_workspace_bytes_not_elements():
+    """A workspace of any dtype is passed with its size in bytes."""
+    import torch
+    assert vd._nbytes(torch.zeros(10, dtype=torch.float32)) == 40
+    assert vd._nbytes(torch.zeros(10, dtype=torch.uint8)) == 10

@@ -15,6 +15,7 @@ import torch
 import oracle
 import oracle_pins as pins
 import paper_2509_04827_amd as vd
+from parity_gates import CANARY_MAX_ABS, CANARY_REL_L2, GATE_MAX_ABS, GATE_REL_L2
 from workloads import ORDER, Workload, bits, make_case
 
 pytestmark = pytest.mark.gpu
@@ -56,13 +57,16 @@ def bf16_ulp(x):
     return np.ldexp(1.0, (e - 7).astype(np.int64))
 
 
-def check_f32(got, ref, what):
+def check_f32(got, ref, what, canary=False):
     got = got.double().cpu().numpy() if isinstance(got, torch.Tensor) else got
     assert np.isfinite(got).all(), "%s: non-finite output" % what
     err = np.abs(got - ref)
     rel = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-300)
     say("%s: fp32 out max-abs %.3e rel-L2 %.3e" % (what, err.max(), rel))
-    assert err.max() <= 1e-2 and rel <= 5e-3, what
+    assert err.max() <= GATE_MAX_ABS and rel <= GATE_REL_L2, what
+    if canary:
+        assert err.max() <= CANARY_MAX_ABS and rel <= CANARY_REL_L2, \
+            "%s: precision canary (max-abs %.3e rel-L2 %.3e)" % (what, err.max(), rel)
     return err.max(), rel
 
 
@@ -92,7 +96,7 @@ def test_workload_parity(name):
     got32 = run_gpu(d, torch.float32)
     got16 = run_gpu(d, torch.bfloat16)
     ref = ref_of(c)
-    check_f32(got32, ref, name)
+    check_f32(got32, ref, name, canary=True)
     check_bf16(got16, ref, name)
 
 
@@ -225,7 +229,7 @@ def test_few_long_requests(lengths):
     c = custom(lengths, seed=20 + len(lengths))
     d = dev_case(c)
     ref = ref_of(c)
-    check_f32(run_gpu(d), ref, "long %s" % lengths)
+    check_f32(run_gpu(d), ref, "long %s" % lengths, canary=True)
     check_bf16(run_gpu(d, torch.bfloat16), ref, "long %s" % lengths)
 
 
@@ -650,7 +654,7 @@ def test_random_shapes(trial):
     c = custom(lengths, hq=G * hkv, hkv=hkv, seed=2000 + trial, pt_stride=stride)
     d = dev_case(c)
     ref = ref_of(c)
-    check_f32(run_gpu(d, flags=flags), ref, "random %d" % trial)
+    check_f32(run_gpu(d, flags=flags), ref, "random %d" % trial, canary=True)
     check_bf16(run_gpu(d, torch.bfloat16, flags=flags), ref, "random %d" % trial)
 
 
@@ -687,7 +691,7 @@ def test_random_sweep(trial):
     d = dev_case(c)
     ref = ref_of(c)
     whole = run_gpu(d, torch.float32, flags=flags)
-    check_f32(whole, ref, what)
+    check_f32(whole, ref, what, canary=True)
     if trial % 4 == 0:
         check_bf16(run_gpu(d, torch.bfloat16, flags=flags), ref, what)
     maxp = d["page_table"].shape[1]
