@@ -67,7 +67,8 @@ typedef enum vd_status {
     VD_ERROR_INVALID_VALUE = 1,       /* NULL pointer, bad size, misalignment, bad flag, non-finite scale */
     VD_ERROR_NOT_SUPPORTED = 2,       /* head_dim, page_size, G, num_seqs or a 32-bit size limit outside the supported set */
     VD_ERROR_WORKSPACE_TOO_SMALL = 3, /* workspace_bytes below vd_decode_workspace_size() */
-    VD_ERROR_LAUNCH = 4               /* a kernel launch failed (hipGetLastError) */
+    VD_ERROR_LAUNCH = 4,              /* a kernel launch failed (hipGetLastError) */
+    VD_ERROR_SCRATCH_LIMIT = 5        /* vd_decode_attn_noalloc: the sizes need more than its fixed scratch */
 } vd_status;
 
 /* flags */
@@ -140,6 +141,35 @@ int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
                    int head_dim, int page_size, float scale,
                    int max_pages_per_seq, void *workspace,
                    size_t workspace_bytes, unsigned flags, hipStream_t stream);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops or harnesses that forbid hipMalloc): the whole step
+ * of vd_decode_attn, same arguments but no workspace.  Its workspace is a
+ * fixed scratch array of VD_NOALLOC_SCRATCH_BYTES inside the library, one per
+ * device (held from the device's first call until the process ends), so the
+ * call allocates nothing, by any route.  The plan is cut for the device's own
+ * number of resident workgroups, as vd_decode_attn's is, so the output equals
+ * vd_decode_attn's bit for bit.
+ * Limit: sizes whose plan and partials need more than the scratch return
+ * VD_ERROR_SCRATCH_LIMIT with nothing enqueued.  The need is about
+ * num_seqs * n_q_heads * 512 B plus ~2 KB per range; on MI355X, 256 requests
+ * of up to 16384 tokens at 32:8 heads take 14 MB and 1024 of them 51 MB,
+ * while 4000 requests at 32 query heads exceed the scratch.
+ * Every call on one device shares that device's scratch and leaves its step
+ * record (vd_step_info) at the scratch's start: calls that overlap on one
+ * device (concurrent streams, host threads) race and must be serialised by
+ * the caller, e.g. kept on one stream.  Nothing in the scratch needs to start
+ * at zero; each call writes what it reads.  Errors as vd_decode_attn, plus
+ * VD_ERROR_SCRATCH_LIMIT; VD_ERROR_LAUNCH also when the scratch's device
+ * address cannot be found.
+ */
+#define VD_NOALLOC_SCRATCH_BYTES (64u << 20)
+int vd_decode_attn_noalloc(const void *q, const void *k_pages, const void *v_pages,
+                           const int32_t *page_table, const int32_t *seq_lens, void *out,
+                           int num_seqs, int n_q_heads, int n_kv_heads, int head_dim,
+                           int page_size, float scale, int max_pages_per_seq, unsigned flags,
+                           hipStream_t stream);
 
 /*
  * Stage 1 of 3: lay every (page, KV head) tile of the step out in one sequence

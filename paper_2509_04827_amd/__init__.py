@@ -34,11 +34,13 @@ VD_ERROR_INVALID_VALUE = 1
 VD_ERROR_NOT_SUPPORTED = 2
 VD_ERROR_WORKSPACE_TOO_SMALL = 3
 VD_ERROR_LAUNCH = 4
+VD_ERROR_SCRATCH_LIMIT = 5
+VD_NOALLOC_SCRATCH_BYTES = 64 << 20
 VD_FLAG_OUT_F32 = 1 << 0
 VD_FLAG_SELF_PLAN = 1 << 1
 VD_FLAG_RANGE_SHIFT = 8
 
-EXPORTS = ("vd_status_string", "vd_decode_workspace_size", "vd_decode_attn", "vd_decode_plan",
+EXPORTS = ("vd_status_string", "vd_decode_workspace_size", "vd_decode_attn", "vd_decode_attn_noalloc", "vd_decode_plan",
            "vd_decode_partial", "vd_decode_combine", "vd_decode_gather", "vd_kv_append", "vd_gemm_workspace_size", "vd_gemm_bf16",
            "vd_stream_read")
 
@@ -72,6 +74,7 @@ def lib() -> ctypes.CDLL:
         attn = [P, P, P, P, P, P, I, I, I, I, I, F, I, P, Z, U, P]
         L.vd_decode_attn.argtypes = attn
         L.vd_decode_partial.argtypes = attn
+        L.vd_decode_attn_noalloc.argtypes = [P, P, P, P, P, P, I, I, I, I, I, F, I, U, P]
         L.vd_decode_plan.argtypes = [P, I, I, I, I, I, I, P, Z, U, P]
         L.vd_decode_combine.argtypes = [P, I, I, I, I, I, I, P, Z, U, P]
         L.vd_decode_gather.argtypes = [P, P, P, P, P, P, I, I, I, I, I, P, Z, P]
@@ -80,7 +83,7 @@ def lib() -> ctypes.CDLL:
         L.vd_gemm_workspace_size.restype = Z
         L.vd_gemm_bf16.argtypes = [P, P, P, I, I, I, P, Z, U, P]
         L.vd_stream_read.argtypes = [P, Z, P, I, P]
-        for n in ("vd_decode_attn", "vd_decode_partial", "vd_decode_plan", "vd_decode_combine",
+        for n in ("vd_decode_attn", "vd_decode_attn_noalloc", "vd_decode_partial", "vd_decode_plan", "vd_decode_combine",
                   "vd_decode_gather", "vd_kv_append", "vd_gemm_bf16", "vd_stream_read"):
             getattr(L, n).restype = I
         # every export has a prototype: pointers travel as plain ints, which
@@ -227,6 +230,19 @@ def vd_decode_attn(q, k_pages, v_pages, page_table, seq_lens, out, scale: float,
                                 _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale), maxp,
                                 _ptr(workspace), _nbytes(workspace), _out_flags(out, flags),
                                 _stream(stream, out)), "vd_decode_attn")
+
+
+def vd_decode_attn_noalloc(q, k_pages, v_pages, page_table, seq_lens, out, scale: float,
+                           flags: int = 0, stream=None) -> None:
+    """vd_decode_attn with the library's fixed scratch as its workspace: the
+    call allocates nothing.  Calls that overlap on one device share that
+    scratch and race."""
+    _attn_dtypes(q, k_pages, v_pages, page_table, seq_lens, out)
+    B, Hq, Hkv, D, S, maxp = _attn_sizes(q, k_pages, v_pages, page_table, seq_lens, out)
+    _check(lib().vd_decode_attn_noalloc(_ptr(q), _ptr(k_pages), _ptr(v_pages), _ptr(page_table),
+                                        _ptr(seq_lens), _ptr(out), B, Hq, Hkv, D, S, float(scale),
+                                        maxp, _out_flags(out, flags), _stream(stream, out)),
+           "vd_decode_attn_noalloc")
 
 
 def vd_decode_plan(seq_lens, n_q_heads: int, n_kv_heads: int, max_pages_per_seq: int, workspace,

@@ -125,15 +125,18 @@ inline int heads_per_group(int Hkv)
 }
 
 // Range capacity.  Automatic plans: W = R * ceil(T / (kMaxRangeTiles * R))
-// with R <= kMaxResidentGroups resident workgroups, so W < R + T /
-// kMaxRangeTiles.  A forced range length c: W = ceil(T / c).
-// T <= B * maxp * Hkv / HW tiles; partial slots (W + B * Hkv / HW) * HW.
-inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced)
+// with R resident workgroups, so W < R + T / kMaxRangeTiles.  A forced range
+// length c: W = ceil(T / c).  T <= B * maxp * Hkv / HW tiles; partial slots
+// (W + B * Hkv / HW) * HW.  The caller-sized workspace takes R at its bound
+// kMaxResidentGroups, so its size does not depend on the device; the
+// no-allocation entry point sizes its fixed scratch with the device's own R.
+inline WsLayout ws_layout(int B, int G, int Hkv, int maxp, int forced,
+                          int resident = kMaxResidentGroups)
 {
     const int HW = heads_per_group(Hkv);
     const long long tiles = (long long)B * maxp * (Hkv / HW);
     long long cap = forced > 0 ? ceil_div_ll(tiles, forced)
-                               : kMaxResidentGroups + ceil_div_ll(tiles, kMaxRangeTiles);
+                               : resident + ceil_div_ll(tiles, kMaxRangeTiles);
     cap = std::max(cap, 1LL);
     const long long slots = cap * HW + (long long)B * Hkv;
     WsLayout l;
@@ -1517,22 +1520,39 @@ int enqueue_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, cons
     return launch_status();
 }
 
+// Sizes, flags, data pointers and scale of an attention call.
+int check_attn_inputs(const void *q, const void *k_pages, const void *v_pages,
+                      const int32_t *page_table, const int32_t *seq_lens, const void *out,
+                      int num_seqs, int n_q_heads, int n_kv_heads, int head_dim, int page_size,
+                      float scale, int max_pages_per_seq, unsigned flags)
+{
+    int st = check_shapes(num_seqs, n_q_heads, n_kv_heads, head_dim, page_size,
+                          max_pages_per_seq, flags);
+    if (st)
+        return st;
+    if (!q || !k_pages || !v_pages || !page_table || !seq_lens || !out)
+        return VD_ERROR_INVALID_VALUE;
+    if (!aligned(q, 16) || !aligned(k_pages, 16) || !aligned(v_pages, 16) || !aligned(out, 16) ||
+        !aligned(page_table, 4) || !aligned(seq_lens, 4))
+        return VD_ERROR_INVALID_VALUE;
+    if (!std::isfinite(scale))
+        return VD_ERROR_INVALID_VALUE;
+    return VD_SUCCESS;
+}
+
+// The same and the caller's workspace.
 int check_attn_args(const void *q, const void *k_pages, const void *v_pages,
                     const int32_t *page_table, const int32_t *seq_lens, const void *out,
                     int num_seqs, int n_q_heads, int n_kv_heads, int head_dim, int page_size,
                     float scale, int max_pages_per_seq, const void *workspace,
                     size_t workspace_bytes, unsigned flags)
 {
-    int st = check_shapes(num_seqs, n_q_heads, n_kv_heads, head_dim, page_size,
-                          max_pages_per_seq, flags);
+    int st = check_attn_inputs(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs,
+                               n_q_heads, n_kv_heads, head_dim, page_size, scale,
+                               max_pages_per_seq, flags);
     if (st)
         return st;
-    if (!q || !k_pages || !v_pages || !page_table || !seq_lens || !out || !workspace)
-        return VD_ERROR_INVALID_VALUE;
-    if (!aligned(q, 16) || !aligned(k_pages, 16) || !aligned(v_pages, 16) || !aligned(out, 16) ||
-        !aligned(workspace, 16) || !aligned(page_table, 4) || !aligned(seq_lens, 4))
-        return VD_ERROR_INVALID_VALUE;
-    if (!std::isfinite(scale))
+    if (!workspace || !aligned(workspace, 16))
         return VD_ERROR_INVALID_VALUE;
     const WsLayout lay = ws_layout(num_seqs, n_q_heads / n_kv_heads, n_kv_heads,
                                    max_pages_per_seq, forced_tiles(flags));
@@ -1548,10 +1568,10 @@ int out_mode(unsigned flags) { return (flags & VD_FLAG_OUT_F32) ? MODE_F32 : MOD
 int enqueue_partial(const void *q, const void *k_pages, const void *v_pages,
                     const int32_t *page_table, const int32_t *seq_lens, void *out, int num_seqs,
                     int n_q_heads, int n_kv_heads, float scale, int max_pages_per_seq,
-                    void *workspace, unsigned flags, bool self, hipStream_t stream)
+                    const WsLayout &lay, void *workspace, unsigned flags, bool self,
+                    hipStream_t stream)
 {
     const int G = n_q_heads / n_kv_heads;
-    const WsLayout lay = ws_layout(num_seqs, G, n_kv_heads, max_pages_per_seq, forced_tiles(flags));
     AttnArgs a = make_args(lay, workspace, num_seqs, n_q_heads, n_kv_heads, max_pages_per_seq,
                            scale, flags);
     a.q = (const uint16_t *)q;
@@ -1561,6 +1581,40 @@ int enqueue_partial(const void *q, const void *k_pages, const void *v_pages,
     a.seq_lens = seq_lens;
     a.out = out;
     return enqueue_attn(a, G, out_mode(flags), self, stream);
+}
+
+// ---------------------------------------------------------------- fixed scratch
+// The workspace of vd_decode_attn_noalloc: one array per device, part of the
+// library's code object, so that entry point allocates nothing.  Host code
+// never uses the array's name as an address (on the host it is a stand-in
+// symbol): its device address is looked up once per device, with that device
+// current, and every kernel argument is taken from there.
+constexpr size_t kNoAllocScratchBytes = (size_t)VD_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+std::atomic<char *> g_scratch[kMaxDevices];
+
+int noalloc_scratch(char **out)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return VD_ERROR_LAUNCH;
+    if (dev >= 0 && dev < kMaxDevices) {
+        char *p = g_scratch[dev].load(std::memory_order_acquire);
+        if (p) {
+            *out = p;
+            return VD_SUCCESS;
+        }
+    }
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+        (void)hipGetLastError();   // leave no sticky error for the caller's next call
+        return VD_ERROR_LAUNCH;
+    }
+    if (dev >= 0 && dev < kMaxDevices)   // concurrent first calls store the same address
+        g_scratch[dev].store((char *)p, std::memory_order_release);
+    *out = (char *)p;
+    return VD_SUCCESS;
 }
 
 }  // namespace
@@ -1576,6 +1630,7 @@ const char *vd_status_string(int status)
     case VD_ERROR_NOT_SUPPORTED: return "VD_ERROR_NOT_SUPPORTED";
     case VD_ERROR_WORKSPACE_TOO_SMALL: return "VD_ERROR_WORKSPACE_TOO_SMALL";
     case VD_ERROR_LAUNCH: return "VD_ERROR_LAUNCH";
+    case VD_ERROR_SCRATCH_LIMIT: return "VD_ERROR_SCRATCH_LIMIT";
     default: return "VD_UNKNOWN_STATUS";
     }
 }
@@ -1623,8 +1678,10 @@ int vd_decode_partial(const void *q, const void *k_pages, const void *v_pages,
         return st;
     if (num_seqs == 0)
         return VD_SUCCESS;
+    const WsLayout lay = ws_layout(num_seqs, n_q_heads / n_kv_heads, n_kv_heads, max_pages_per_seq,
+                                   forced_tiles(flags));
     return enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
-                           n_kv_heads, scale, max_pages_per_seq, workspace, flags,
+                           n_kv_heads, scale, max_pages_per_seq, lay, workspace, flags,
                            (flags & VD_FLAG_SELF_PLAN) != 0, stream);
 }
 
@@ -1661,13 +1718,48 @@ int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
     if (num_seqs == 0)
         return VD_SUCCESS;
     // self-planned attention, then the combine kernel
-    st = enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
-                         n_kv_heads, scale, max_pages_per_seq, workspace, flags, true, stream);
-    if (st)
-        return st;
     const WsLayout lay = ws_layout(num_seqs, n_q_heads / n_kv_heads, n_kv_heads, max_pages_per_seq,
                                    forced_tiles(flags));
+    st = enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
+                         n_kv_heads, scale, max_pages_per_seq, lay, workspace, flags, true, stream);
+    if (st)
+        return st;
     return enqueue_combine(out, num_seqs, n_q_heads, n_kv_heads, lay, workspace, flags, stream);
+}
+
+int vd_decode_attn_noalloc(const void *q, const void *k_pages, const void *v_pages,
+                           const int32_t *page_table, const int32_t *seq_lens, void *out,
+                           int num_seqs, int n_q_heads, int n_kv_heads, int head_dim,
+                           int page_size, float scale, int max_pages_per_seq, unsigned flags,
+                           hipStream_t stream)
+{
+    // the checks of vd_decode_attn but the workspace's: the fixed scratch
+    // replaces it, sized below
+    int st = check_attn_inputs(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs,
+                               n_q_heads, n_kv_heads, head_dim, page_size, scale,
+                               max_pages_per_seq, flags);
+    if (st)
+        return st;
+    if (num_seqs == 0)
+        return VD_SUCCESS;
+    const int G = n_q_heads / n_kv_heads;
+    int groups = 0;
+    st = resident_attn_groups(G, out_mode(flags), heads_per_group(n_kv_heads), &groups);
+    if (st)
+        return st;
+    const WsLayout lay = ws_layout(num_seqs, G, n_kv_heads, max_pages_per_seq, forced_tiles(flags),
+                                   groups);
+    if (lay.total > kNoAllocScratchBytes)
+        return VD_ERROR_SCRATCH_LIMIT;
+    char *ws = nullptr;
+    st = noalloc_scratch(&ws);
+    if (st)
+        return st;
+    st = enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
+                         n_kv_heads, scale, max_pages_per_seq, lay, ws, flags, true, stream);
+    if (st)
+        return st;
+    return enqueue_combine(out, num_seqs, n_q_heads, n_kv_heads, lay, ws, flags, stream);
 }
 
 int vd_decode_gather(const void *k_pages, const void *v_pages, const int32_t *page_table,

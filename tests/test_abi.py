@@ -122,6 +122,31 @@ def test_plan_combine_gather_argument_errors():
                               None) == vd.VD_ERROR_NOT_SUPPORTED
 
 
+def test_noalloc_argument_errors():
+    """vd_decode_attn_noalloc checks its arguments as vd_decode_attn does
+    (minus the workspace) before it looks at the device."""
+    fn = vd.lib().vd_decode_attn_noalloc
+
+    def call(**kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, pt=FAKE, sl=FAKE, out=FAKE, B=4, Hq=32, Hkv=8, D=128,
+                 S=16, scale=0.088, maxp=63, flags=0, stream=None)
+        a.update(kw)
+        return fn(a["q"], a["k"], a["v"], a["pt"], a["sl"], a["out"], a["B"], a["Hq"], a["Hkv"],
+                  a["D"], a["S"], a["scale"], a["maxp"], a["flags"], a["stream"])
+
+    assert call(q=None) == vd.VD_ERROR_INVALID_VALUE
+    assert call(out=MIS) == vd.VD_ERROR_INVALID_VALUE
+    assert call(scale=float("nan")) == vd.VD_ERROR_INVALID_VALUE
+    assert call(flags=1 << 7) == vd.VD_ERROR_INVALID_VALUE
+    assert call(D=64) == vd.VD_ERROR_NOT_SUPPORTED
+    assert call(B=9000) == vd.VD_ERROR_NOT_SUPPORTED
+    assert call(B=0) == vd.VD_SUCCESS              # nothing to do, nothing enqueued
+    assert vd.vd_status_string(vd.VD_ERROR_SCRATCH_LIMIT) == "VD_ERROR_SCRATCH_LIMIT"
+    hdr = open(os.path.join(ROOT, "include", "vdecode.h")).read()
+    assert vd.VD_NOALLOC_SCRATCH_BYTES == int(re.search(r"VD_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", hdr).group(1)) << \
+        int(re.search(r"VD_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", hdr).group(2))
+
+
 def test_append_and_stream_argument_errors():
     L = vd.lib()
     assert L.vd_kv_append(None, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 8, 128, 16, 63, None) == vd.VD_ERROR_INVALID_VALUE
