@@ -17,8 +17,10 @@ Prints one JSON line:
                 MI355X's 8 TB/s; traffic from the committed FETCH_SIZE /
                 WRITE_SIZE counter summary when it matches this kernel source
   cpu_baseline  the fp64 oracle on the host cores over the same workload
-  cold_cache    step times with a 1 GiB cache flush before each step
-                (p10 / median / p90), outside the back-to-back timing
+  cold_cache    step times with the caches flushed (a 1 GiB read) before
+                each step, one step at a time: p10 / median / p90 of the
+                step and of its attention launch, outside the back-to-back
+                timing
 """
 from __future__ import annotations
 
@@ -315,6 +317,7 @@ GEMM_SHAPES = (("qkv", 6144, 4096), ("o_proj", 4096, 4096), ("gate_up", 28672, 4
                ("down", 4096, 14336))
 GEMM_M = (1, 2, 4, 8, 16, 24, 32, 48, 64, 96, 128, 160, 192, 224, 240, 248, 255, 256, 257, 264,
           272, 288, 320, 384, 448, 512, 513, 640, 768, 1024)
+NEXT_PROFILE_M = (1, 16, 64, 256, 257, 1024)
 
 
 def clock_sweep(outdir: str, bursts: int = 10, steps: int = 60, idle_s: float = 1.5):
@@ -419,9 +422,13 @@ def clock_sweep(outdir: str, bursts: int = 10, steps: int = 60, idle_s: float = 
 
 def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
     """Decode-step projection GEMMs of a Llama-3-8B-shaped layer (hidden 4096,
-    KV 8 x 128, MLP 14336) over the decode batch M: this library's
-    weight-streaming kernel (M <= 64) against torch.matmul (hipBLASLt), to
-    locate the batch steps the paper traces to tile quantisation (Sec. 3.3)."""
+    KV 8 x 128, MLP 14336) over the decode batch M: this library's tiled
+    kernel against torch.matmul (hipBLASLt), to locate the batch steps the
+    paper traces to tile quantisation (Sec. 3.3).  Primary timing is with
+    cold weights: each call reads the next of a ring of weight copies that
+    together exceed 1 GiB, so neither L2 nor the 256 MB Infinity Cache holds
+    them (in a decode step each layer's weights are read once); warm timing
+    (one copy, re-read) beside it."""
     import numpy as np
     import torch
 
@@ -434,40 +441,45 @@ def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
     rows = []
 
     def timed(fn):
-        settle_clocks(fn, 0.02)
-        for _ in range(warmup):
-            fn()
+        settle_clocks(lambda: fn(0), 0.02)
+        for i in range(warmup):
+            fn(i)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record(stream)
-        for _ in range(iters):
-            fn()
+        for i in range(iters):
+            fn(i)
         e1.record(stream)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / iters
 
     for name, N, K in GEMM_SHAPES:
-        w = torch.randn((N, K), generator=gen, device=dev).to(torch.bfloat16)
+        ring_n = max(2, -(-(1 << 30) // (N * K * 2)))
+        ring = [torch.randn((N, K), generator=gen, device=dev).to(torch.bfloat16) for _ in range(ring_n)]
         for M in GEMM_M:
             x = torch.randn((M, K), generator=gen, device=dev).to(torch.bfloat16)
             y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
-            us_lib = timed(lambda: torch.matmul(x, w.t(), out=y))
-            us_own = None
-            if M <= 64:
-                ws = torch.empty(max(16, vd.vd_gemm_workspace_size(M, N, K)), dtype=torch.uint8,
-                                 device=dev)
-                us_own = timed(lambda: vd.vd_gemm_bf16(x, w, y, ws, stream=stream))
+            ws = torch.empty(max(16, vd.vd_gemm_workspace_size(M, N, K)), dtype=torch.uint8, device=dev)
+            us_lib = timed(lambda i: torch.matmul(x, ring[i % ring_n].t(), out=y))
+            us_own = timed(lambda i: vd.vd_gemm_bf16(x, ring[i % ring_n], y, ws, stream=stream))
+            us_lib_warm = timed(lambda i: torch.matmul(x, ring[0].t(), out=y))
+            us_own_warm = timed(lambda i: vd.vd_gemm_bf16(x, ring[0], y, ws, stream=stream))
             nbytes = (N * K + M * K + M * N) * 2
             flops = 2.0 * M * N * K
             floor_us = max(nbytes / (PEAK_HBM_GBS * 1e3), flops / 2.5e9)
             rows.append(dict(shape=name, M=M, N=N, K=K, us_hipblaslt=round(us_lib, 2),
-                             us_own=None if us_own is None else round(us_own, 2),
-                             roofline_us=round(floor_us, 2),
+                             us_own=round(us_own, 2), roofline_us=round(floor_us, 2),
                              gbs_hipblaslt=round(nbytes / us_lib / 1e3, 1),
-                             gbs_own=None if us_own is None else round(nbytes / us_own / 1e3, 1)))
-            print("gemm %-8s M %5d N %6d K %6d  hipBLASLt %8.2f us  own %8s us  roofline %6.2f us"
-                  % (name, M, N, K, us_lib, "-" if us_own is None else "%.2f" % us_own, floor_us),
+                             gbs_own=round(nbytes / us_own / 1e3, 1),
+                             tflops_own=round(flops / us_own / 1e6, 1),
+                             us_hipblaslt_warm=round(us_lib_warm, 2), us_own_warm=round(us_own_warm, 2),
+                             workspace_bytes=vd.vd_gemm_workspace_size(M, N, K)))
+            print("gemm %-8s M %5d N %6d K %6d  cold: hipBLASLt %8.2f own %8.2f us  warm: %8.2f %8.2f  roofline %6.2f us"
+                  % (name, M, N, K, us_lib, us_own, us_lib_warm, us_own_warm, floor_us),
                   file=sys.stderr, flush=True)
+            del x, y, ws
+        del ring
+        torch.cuda.empty_cache()
     os.makedirs(outdir, exist_ok=True)
     keys = list(rows[0].keys())
     with open(os.path.join(outdir, "decode_gemm_sweep.csv"), "w") as f:
@@ -479,7 +491,8 @@ def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
 
 def next_profile(outdir: str, iters: int = 20, warmup: int = 3):
     """A short, profiler-friendly run of the other kernels: vd_gemm_bf16 on
-    the four Llama-3-8B-shaped projections at M = 1, 16 and 64, then
+    the four Llama-3-8B-shaped projections at M = 1, 16, 64, 256, 257 and
+    1024 (cold weights: a ring of copies over 1 GiB), then
     vd_kv_append on the chat batch's sizes (256 requests, 8 KV heads).  Each
     case is a burst of `iters` calls after `warmup` calls, with a 5 ms pause
     before it, so a kernel trace splits into one burst per case in the order
@@ -516,15 +529,24 @@ def next_profile(outdir: str, iters: int = 20, warmup: int = 3):
         return e0.elapsed_time(e1) * 1e3 / iters
 
     for name, N, K in GEMM_SHAPES:
-        w = torch.randn((N, K), generator=gen, device=dev).to(torch.bfloat16)
-        for M in (1, 16, 64):
+        # a ring of weight copies over 1 GiB: every call reads weights that
+        # no cache holds, as a decode step does
+        ring_n = max(2, -(-(1 << 30) // (N * K * 2)))
+        ring = [torch.randn((N, K), generator=gen, device=dev).to(torch.bfloat16) for _ in range(ring_n)]
+        for M in NEXT_PROFILE_M:
             x = torch.randn((M, K), generator=gen, device=dev).to(torch.bfloat16)
             y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
             ws = torch.empty(max(16, vd.vd_gemm_workspace_size(M, N, K)), dtype=torch.uint8, device=dev)
-            us = burst(lambda: vd.vd_gemm_bf16(x, w, y, ws, stream=stream))
+            cnt = [0]
+
+            def call():
+                vd.vd_gemm_bf16(x, ring[cnt[0] % ring_n], y, ws, stream=stream)
+                cnt[0] += 1
+            us = burst(call)
             rows.append(dict(case="gemm_%s_M%d" % (name, M), calls=iters, us_events=round(us, 2),
                              algorithmic_bytes=(N * K + M * K + M * N) * 2))
-        del w
+        del ring
+        torch.cuda.empty_cache()
     B, Hkv, S, maxp = 256, 8, 16, 4
     pages = torch.randperm(B * maxp, generator=torch.Generator().manual_seed(1)).to(torch.int32)
     pt = pages.view(B, maxp).to(dev)
@@ -555,6 +577,8 @@ def main():
     ap.add_argument("--workload", default=WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-cold", action="store_true", help="skip the flushed-cache step timings")
+    ap.add_argument("--flushed", type=int, default=50, metavar="N",
+                    help="flushed-cache steps timed one at a time (default 50)")
     ap.add_argument("--no-ceiling", action="store_true", help="skip the HBM read-ceiling run")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the oracle over the whole step for this much wall time "
@@ -569,7 +593,7 @@ def main():
                     help="instead of the bench line, time the attention kernel against the "
                          "shader clock it ran at and write DIR/decode_clock_sweep.{csv,json}")
     ap.add_argument("--next-profile", metavar="DIR", default=None,
-                    help="short run of the GEMM (4 shapes x M 1/16/64) and KV-append kernels "
+                    help="short run of the GEMM (4 shapes x M 1/16/64/256/257/1024) and KV-append kernels "
                          "for a kernel trace; writes next_profile.csv to DIR")
     ap.add_argument("--cpu-configs", metavar="DIR", default=None,
                     help="time the oracle on the host cores and the GPU on every seeded workload; "
@@ -688,32 +712,51 @@ def main():
     torch.cuda.synchronize()
     attn_avg_ms = a0.elapsed_time(a1) / K
 
-    # Cold caches: a 1 GiB write (beyond the 256 MB Infinity Cache and the
-    # L2s) before each step; per-step events, outside the back-to-back timing.
+    # Flushed caches (the measurement protocol's primary timing): before each
+    # step, a read of a 1 GiB buffer (vd_stream_read) evicts the 256 MB
+    # Infinity Cache and the L2s without leaving dirty lines behind; then the
+    # step alone between events, one step at a time (a host synchronisation
+    # between steps).  The same with a 1 GiB write as the flush is kept for
+    # comparison: the write's dirty lines are written back while the step
+    # runs, which slows it.  Untimed: the flushes.
     cold = None
     if not args.no_cold:
-        flush = torch.empty(1 << 28, dtype=torch.int32, device=dev)
-        steps_us, attn_us = [], []
-        for _ in range(max(10, K // 2)):
-            flush.zero_()
-            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-            e[0].record(stream)
-            step()
-            e[1].record(stream)
-            torch.cuda.synchronize()
-            steps_us.append(e[0].elapsed_time(e[1]) * 1e3)
-        for _ in range(max(10, K // 2)):
-            flush.zero_()
-            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-            step(e[0], e[1])
-            torch.cuda.synchronize()
-            attn_us.append(e[0].elapsed_time(e[1]) * 1e3)
-        del flush
-        p10, p50, p90 = np.percentile(steps_us, [10, 50, 90])
-        cold = {"flush_bytes": 1 << 30, "us_per_step_p10": round(float(p10), 2),
-                "us_per_step_median": round(float(p50), 2), "us_per_step_p90": round(float(p90), 2),
-                "attn_us_median": round(float(np.median(attn_us)), 2),
-                "kv_gbs_median": round(kv_bytes(c) / (p50 * 1e-6) / 1e9, 2)}
+        fbuf = torch.zeros(1 << 30, dtype=torch.uint8, device=dev)
+        fsink = torch.zeros(4, dtype=torch.int32, device=dev)
+
+        def read_flush():
+            vd.vd_stream_read(fbuf, fsink, stream=stream)
+
+        def write_flush():
+            fbuf.zero_()
+
+        def flushed(flush, attn_only_events, n):
+            out = []
+            for _ in range(n):
+                flush()
+                e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                if attn_only_events:
+                    step(e[0], e[1])
+                else:
+                    e[0].record(stream)
+                    step()
+                    e[1].record(stream)
+                torch.cuda.synchronize()
+                out.append(e[0].elapsed_time(e[1]) * 1e3)
+            return np.percentile(out, [10, 50, 90])
+
+        n = args.flushed
+        sp = flushed(read_flush, False, n)
+        ap_ = flushed(read_flush, True, n)
+        wp = flushed(write_flush, False, max(10, n // 5))
+        del fbuf, fsink
+        cold = {"flush": "read of 1 GiB before each step", "steps": n,
+                "us_per_step_p10": round(float(sp[0]), 2), "us_per_step_median": round(float(sp[1]), 2),
+                "us_per_step_p90": round(float(sp[2]), 2),
+                "attn_us_p10": round(float(ap_[0]), 2), "attn_us_median": round(float(ap_[1]), 2),
+                "attn_us_p90": round(float(ap_[2]), 2),
+                "kv_gbs_median": round(kv_bytes(c) / (sp[1] * 1e-6) / 1e9, 2),
+                "write_flush_us_per_step_median": round(float(wp[1]), 2)}
 
     # HBM read ceiling on this device: vd_stream_read over 4 GiB.
     ceiling = None

@@ -257,12 +257,26 @@ int vd_kv_append(const void *k_new, const void *v_new, void *k_pages,
  * charges to N_req, Sec. 5.4, Eq. pred-itl; its batch steps, Sec. 3.3).
  *   x  bf16 [M][K], row-major           w  bf16 [N][K] (a linear layer's weight)
  *   y  bf16 (RNE) or fp32 with VD_FLAG_OUT_F32, [M][N]
- * fp32 accumulation; the result does not depend on the device (fixed
- * reduction order).  Supported: 1 <= M <= 64, N a multiple of 64, K a
- * multiple of 512.  x, w, y, workspace 16-byte aligned.  The workspace
- * (vd_gemm_workspace_size) holds fp32 partials when K is split across
- * workgroups; it may be NULL when that size is 0.  Errors as above.
+ * fp32 accumulation.  The tile shape and the number of K slices follow from
+ * (M, N, K) alone, so the result is the same on every device and run (fixed
+ * reduction order).  Supported: M >= 1, N a multiple of 64, K a multiple of
+ * 512, M * N < 2^31.  x, w, y, workspace 16-byte aligned.  The workspace
+ * (vd_gemm_workspace_size, same flags) holds fp32 partials when K is split
+ * across workgroups; it may be NULL when that size is 0.  Errors as above;
+ * VD_ERROR_NOT_SUPPORTED also for a forced tile or slice count that does not
+ * fit the sizes.
+ * Flags for tests and sweeps (0 = the automatic choice): VD_GEMM_FLAG_TILE(c)
+ * forces tile configuration c (0..7: BM x BN = 16x64, 32x64, 48x64, 64x64,
+ * 64x128, 128x64, 128x128, 256x128; the last four need N % 128 == 0 where
+ * BN = 128), VD_GEMM_FLAG_SLICES_LOG2(l) forces 2^l K slices (l <= 4).
+ * These bits mean something else for the attention calls.
  */
+#define VD_GEMM_FLAG_TILE_SHIFT 8u
+#define VD_GEMM_FLAG_TILE_MASK (0xFu << VD_GEMM_FLAG_TILE_SHIFT)
+#define VD_GEMM_FLAG_TILE(c) ((((unsigned)(c) + 1u) & 0xFu) << VD_GEMM_FLAG_TILE_SHIFT)
+#define VD_GEMM_FLAG_SLICES_SHIFT 12u
+#define VD_GEMM_FLAG_SLICES_MASK (0xFu << VD_GEMM_FLAG_SLICES_SHIFT)
+#define VD_GEMM_FLAG_SLICES_LOG2(l) ((((unsigned)(l) + 1u) & 0xFu) << VD_GEMM_FLAG_SLICES_SHIFT)
 size_t vd_gemm_workspace_size(int M, int N, int K, unsigned flags);
 int vd_gemm_bf16(const void *x, const void *w, void *y, int M, int N, int K,
                  void *workspace, size_t workspace_bytes, unsigned flags,

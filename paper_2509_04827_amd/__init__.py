@@ -49,6 +49,20 @@ def VD_FLAG_RANGE_TILES(n: int) -> int:
     return (int(n) & 0xFF) << VD_FLAG_RANGE_SHIFT
 
 
+VD_GEMM_FLAG_TILE_SHIFT = 8
+VD_GEMM_FLAG_SLICES_SHIFT = 12
+
+
+def VD_GEMM_FLAG_TILE(c: int) -> int:
+    """vd_gemm_bf16: force tile configuration c (0..7)."""
+    return ((int(c) + 1) & 0xF) << VD_GEMM_FLAG_TILE_SHIFT
+
+
+def VD_GEMM_FLAG_SLICES_LOG2(l: int) -> int:
+    """vd_gemm_bf16: force 2^l K slices (l <= 4)."""
+    return ((int(l) + 1) & 0xF) << VD_GEMM_FLAG_SLICES_SHIFT
+
+
 class VdError(RuntimeError):
     def __init__(self, status: int, where: str):
         super().__init__("%s returned %d (%s)" % (where, status, vd_status_string(status)))

@@ -20,14 +20,17 @@ HIPCC_FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     # packed fp32 VALU forms are kept out of the generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # MFMA accumulators in ordinary VGPRs: the online-softmax rescale touches
-    # them with VALU ops, which would otherwise copy AGPRs back and forth
-    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall",
 ]
+# per source: the attention kernels keep MFMA accumulators in ordinary VGPRs
+# (the online-softmax rescale touches them with VALU ops, which would
+# otherwise copy AGPRs back and forth); the GEMM's large tiles need the AGPRs
+SRC_FLAGS = {
+    "vdecode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "gemm.hip": [],
+}
 
 
 def hipcc() -> str:
@@ -37,9 +40,7 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, *SRCS]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -49,7 +50,25 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed (%d):\n%s" % (res.returncode, err))
     if err.strip() and verbose:
         print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile each source with its flags, then link the shared library."""
+    tag = ".tmp%d" % os.getpid()
+    objs = []
+    try:
+        for src in SRCS:
+            obj = os.path.join(HERE, os.path.basename(src) + tag + ".o")
+            objs.append(obj)
+            _run([hipcc(), *HIPCC_FLAGS, *SRC_FLAGS[os.path.basename(src)], "-I",
+                  os.path.join(ROOT, "include"), "-c", "-o", obj, src], verbose)
+        tmp = LIB + tag
+        _run([hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs], verbose)
+        os.replace(tmp, LIB)
+    finally:
+        for obj in objs:
+            if os.path.exists(obj):
+                os.remove(obj)
     return LIB
 
 

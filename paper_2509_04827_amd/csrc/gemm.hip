@@ -1,27 +1,37 @@
-// Decode-step projection GEMM for MI355X (gfx950): y = x . w^T with few rows.
+// Decode-step projection GEMM for MI355X (gfx950): y = x . w^T for a decode
+// batch of M rows.
 //
 // A decode iteration multiplies the N_req current tokens by every weight
-// matrix of the model; the paper charges this GEMM work to N_req in its
-// decode latency model (Sec. 5.4, Eq. pred-itl) and traces the latency steps
-// it sees at batch 256 -> 257 to GEMM tile quantisation (Sec. 3.3).  For
-// decode batches up to 64 rows the GEMM reads far more weight bytes than it
-// does arithmetic (2*M flop per weight element, against ~312 flop/B of MFMA
-// to HBM balance), so this kernel streams the weights once at HBM speed:
+// matrix of the model; the paper charges this GEMM work to N_req in its decode
+// latency model (Sec. 5.4, Eq. pred-itl) and traces the latency steps it sees
+// at batch 256 -> 257 to GEMM tile quantisation (Sec. 3.3).  Up to a few
+// hundred rows the GEMM is bound by reading the weights (2*M flop per weight
+// element against ~312 flop/B of MFMA-to-HBM balance); past that, by the
+// matrix cores.  One tiled kernel covers both:
 //
-//   * a workgroup owns 16 * NB output columns (NB 16-column MFMA blocks: 1
-//     for batches up to 8 rows, 4 above, where the x rows are re-read less
-//     often) and a slice of K; its four waves (eight when 16-column tiles
-//     number at most one per CU) split the slice and merge their
-//     accumulators in LDS in a fixed order;
-//   * a wave loads the weight rows in whole 128-byte pieces (8 rows per
-//     instruction, 8 lanes per row) and moves them through its own LDS tile
-//     into the B operand of v_mfma_f32_16x16x32_bf16 (lane = output column):
-//     the operand layout itself would read 64 bytes per row per instruction,
-//     which streams 20-35% slower.  x rows go straight into the A operand
-//     (lane = batch row).  Four K steps per batch, two batches in flight;
-//   * when there are too few column tiles to fill the device, K is split
-//     over workgroups as well; each slice writes an fp32 partial and a second
-//     kernel adds the slices in order (deterministic, no atomics).
+//   * a workgroup of four waves owns a BM x BN output tile and a K slice; the
+//     x and w tiles of each K stage (BK columns) are loaded with 16-byte loads
+//     (whole 128- or 256-byte row pieces) into registers, and from there into
+//     one of two LDS buffers (rows padded by 16 bytes against bank
+//     conflicts), P stages ahead of the one being multiplied;
+//   * each wave multiplies its (BN/WN) x (BM/WM) part of the tile with
+//     v_mfma_f32_16x16x32_bf16, the w fragment as the A operand (lane = output
+//     column) and the x fragment as B (lane = batch row), so the accumulator
+//     holds four consecutive output columns of one row per lane and the
+//     stores are 16 (fp32) or 8 (bf16) bytes wide;
+//   * w is streamed past the caches when one row tile covers the batch (each
+//     element is read once); x is re-read by every column tile and stays in
+//     L2;
+//   * the tiles that share a w tile (same columns, other rows) are given
+//     workgroup indices that land on the same XCD at about the same time
+//     (workgroups are dealt to the 8 XCDs round-robin), so w comes from HBM
+//     once and from that XCD's L2 for the others;
+//   * when the tiles cannot fill the device, K is split into S slices over
+//     workgroups; each slice writes an fp32 partial and a second kernel adds
+//     the slices in order (deterministic, no atomics).
+//
+// The tile shape and S follow from (M, N, K) alone (a table tuned on MI355X),
+// so the result and the workspace size do not depend on the device.
 //
 // x bf16 [M][K], w bf16 [N][K] (a linear layer's weight), y bf16 (RNE) or
 // fp32 [M][N]; fp32 accumulation.
@@ -29,7 +39,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <atomic>
+#include <cmath>
 #include <stdint.h>
 
 #include "vdecode.h"
@@ -38,28 +48,27 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kTileN = 64;                    // column granularity of N (the widest tile)
-constexpr int kKStep = 32;                    // K per MFMA
-constexpr int kUnroll = 4;                    // K steps per load batch (the LDS tile assumes 4)
-constexpr int kBatchK = kKStep * kUnroll;     // 128
-constexpr int kSliceAlign = 4 * kBatchK;      // K slice granularity: 512 (four waves x one batch)
-constexpr int kMaxM = 64;
+constexpr int kThreads = 256;                 // four waves per workgroup
+constexpr int kNAlign = 64;                   // N granularity
+constexpr int kKAlign = 512;                  // K granularity
 constexpr int kReduceThreads = 256;
-constexpr int kGemmGroupsPerCU = 1;           // split K until this many workgroups exist
+constexpr int kTargetCUs = 256;               // MI355X compute units: the tile table's target
+constexpr int kMaxSlicesLog2 = 4;             // at most 16 K slices
+
+enum { OUT_BF16 = 0, OUT_F32 = 1, OUT_PART = 2 };
 
 struct GemmArgs {
     const uint16_t *x, *w;
     void *y;
-    float *part;
-    int M, N, K, kslice;
-};
-
-template <int NB, int MB>
-struct Batch {
-    u32x4 w[NB][kUnroll];
-    u32x4 x[MB][kUnroll];
+    float *part;          // [S][M][N] fp32 partials when S > 1
+    int M, N, K;
+    int kslice;           // K columns per slice
+    int S;                // slices
+    int tiles_m;          // row tiles
+    int groups;           // column tiles * S
 };
 
 __device__ inline unsigned short bf16_rne(float f)
@@ -67,232 +76,349 @@ __device__ inline unsigned short bf16_rne(float f)
     return __builtin_bit_cast(unsigned short, (__bf16)f);
 }
 
-// MODE 0: bf16 y, 1: fp32 y, 2: fp32 partial per K slice.  WAVES waves split
-// the K slice (4, or 8 when there are few column tiles).
-template <int NB, int MB, int MODE, int WAVES>
-__global__ void __launch_bounds__(64 * WAVES)
-gemm_kernel(const GemmArgs a)
+// One tile configuration: BM x BN output tile, BK columns of K per stage,
+// waves WM (rows) x WN (columns), P stages of loads in flight.  NT: w is
+// loaded past the caches (one row tile reads each w tile once); without it,
+// the row tiles that share a w tile find it in L2.
+template <int BM, int BN, int BK, int WM, int WN, int P, int MODE, bool NT = true>
+__global__ void __launch_bounds__(kThreads)
+gemm_tile_kernel(const GemmArgs a)
 {
-    constexpr int kNB = NB;
-    __shared__ f32x4 red[WAVES - 1][kNB * MB][64];
-    // per wave: the batch's weight rows, 16 rows x 256 B (+16 B against bank
-    // conflicts on the column reads) per block
-    static_assert(kUnroll == 4, "two row halves x two K halves per block");
-    __shared__ u32x4 wst[WAVES][kNB][16][4 * kUnroll + 1];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int r = lane & 15, grp = lane >> 4;
-    const int n0 = blockIdx.x * 16 * kNB;
-    const int slice = blockIdx.y;
-    const int kw = a.kslice / WAVES;
-    const int kb = slice * a.kslice + wave * kw;
-    const int K = a.K, M = a.M;
+    constexpr int CPR = BK / 8;                  // 16-byte chunks per row and stage
+    constexpr int RS = BK + 8;                   // LDS row stride in bf16 (16-byte pad)
+    constexpr int RPL = kThreads / CPR;          // rows one load instruction covers (all threads)
+    constexpr int LX = BM / RPL, LW = BN / RPL;  // loads per thread and stage
+    constexpr int TM = BM / WM, TN = BN / WN;    // a wave's rows and columns
+    constexpr int FM = TM / 16, FN = TN / 16;    // its 16 x 16 blocks
+    static_assert(WM * WN == kThreads / 64, "four waves");
+    static_assert(BM % RPL == 0 && BN % RPL == 0 && LX >= 1 && LW >= 1, "whole loads");
+    static_assert(TM % 16 == 0 && TN % 16 == 0 && BK % 32 == 0, "whole MFMA blocks");
+    __shared__ __attribute__((aligned(16))) uint16_t lds[2][(BM + BN) * RS];
 
-    // loads: instruction (h, c) of a block reads rows 8h .. 8h+7, 128 B each
-    // (k 64c .. 64c+63 of the batch), lane l: row 8h + l/8, k 64c + 8 (l % 8)
-    const uint16_t *wp[kNB][2];
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb)
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-            wp[nb][h] = a.w + (size_t)(n0 + 16 * nb + 8 * h + (lane >> 3)) * K + kb + 8 * (lane & 7);
-    const uint16_t *xp[MB];
-    bool xv[MB];
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-        xv[mb] = 16 * mb + r < M;
-        xp[mb] = a.x + (size_t)(xv[mb] ? 16 * mb + r : 0) * K + kb + 8 * grp;
+    // tile of this workgroup: the tiles_m row tiles of one group (column
+    // tile, slice) sit 8 indices apart, within one window of 8 * tiles_m
+    const int i = blockIdx.x, TMc = a.tiles_m, G = a.groups;
+    const int full = G / 8 * 8;
+    int tm, g;
+    if (i < full * TMc) {
+        const int sg = i / (8 * TMc), rem = i - sg * 8 * TMc;
+        tm = rem >> 3;
+        g = sg * 8 + (rem & 7);
+    } else {
+        const int j = i - full * TMc, r8 = G - full;
+        tm = j / r8;
+        g = full + (j - tm * r8);
     }
+    const int tn = g / a.S, s = g - tn * a.S;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int M = a.M, N = a.N, K = a.K;
+    const int nk = a.kslice / BK;
 
-    auto load = [&](Batch<kNB, MB> &B, int koff) {
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int lrow = t / CPR, lc = (t % CPR) * 8;   // this thread's load row and column
+    const uint16_t *xp = a.x + (size_t)min(m0 + lrow, M - 1) * K + (size_t)s * a.kslice + lc;
+    const uint16_t *wp = a.w + (size_t)(n0 + lrow) * K + (size_t)s * a.kslice + lc;
+    const size_t xstep = (size_t)RPL * K;           // next load's rows
+    // rows past M repeat row M - 1 (loaded, never stored)
+    int xrow_ok[LX];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
+    for (int l = 0; l < LX; ++l)
+        xrow_ok[l] = m0 + lrow + l * RPL < M;
+
+    u32x4 rx[P][LX], rw[P][LW];
+    auto load = [&](u32x4 (&ox)[LX], u32x4 (&ow)[LW], int kt) {
+        const size_t off = (size_t)min(kt, nk - 1) * BK;   // past the end: the last stage again
 #pragma unroll
-            for (int nb = 0; nb < kNB; ++nb)
-                B.w[nb][u] = __builtin_nontemporal_load(
-                    (const u32x4 *)(wp[nb][u & 1] + koff + 64 * (u >> 1)));
+        for (int l = 0; l < LX; ++l)
+            ox[l] = *(const u32x4 *)(xrow_ok[l] ? xp + l * xstep + off : xp + off);
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
+        for (int l = 0; l < LW; ++l) {
+            if constexpr (NT)
+                ow[l] = __builtin_nontemporal_load((const u32x4 *)(wp + l * xstep + off));
+            else
+                ow[l] = *(const u32x4 *)(wp + l * xstep + off);
+        }
+    };
+    auto store = [&](const u32x4 (&ox)[LX], const u32x4 (&ow)[LW], int buf) {
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-                B.x[mb][u] = xv[mb] ? *(const u32x4 *)(xp[mb] + koff + kKStep * u)
-                                    : u32x4{0u, 0u, 0u, 0u};
+        for (int l = 0; l < LX; ++l)
+            *(u32x4 *)&lds[buf][(lrow + l * RPL) * RS + lc] = ox[l];
+#pragma unroll
+        for (int l = 0; l < LW; ++l)
+            *(u32x4 *)&lds[buf][(BM + lrow + l * RPL) * RS + lc] = ow[l];
     };
 
-    f32x4 acc[kNB][MB];
+    f32x4 acc[FN][FM];
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb)
+    for (int fn = 0; fn < FN; ++fn)
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-            acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int fm = 0; fm < FM; ++fm)
+            acc[fn][fm] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    auto compute = [&](const Batch<kNB, MB> &B) {
-        // through LDS into the B-operand layout: lane (r, grp) of K step u
-        // takes row r, 16-byte chunk 4u + grp
+    const int wn = wave % WN, wm = wave / WN;
+    const int r = lane & 15, kq = lane >> 4;
+    auto compute = [&](int buf) {
+        const uint16_t *base = lds[buf];
 #pragma unroll
-        for (int nb = 0; nb < kNB; ++nb)
+        for (int u = 0; u < BK / 32; ++u) {
+            u32x4 af[FN], bfr[FM];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                wst[wave][nb][8 * (u & 1) + (lane >> 3)][8 * (u >> 1) + (lane & 7)] = B.w[nb][u];
+            for (int fn = 0; fn < FN; ++fn)
+                af[fn] = *(const u32x4 *)(base + (BM + wn * TN + 16 * fn + r) * RS + 32 * u + 8 * kq);
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
+            for (int fm = 0; fm < FM; ++fm)
+                bfr[fm] = *(const u32x4 *)(base + (wm * TM + 16 * fm + r) * RS + 32 * u + 8 * kq);
 #pragma unroll
-            for (int nb = 0; nb < kNB; ++nb) {
-                const u32x4 wf = wst[wave][nb][r][4 * u + grp];
+            for (int fn = 0; fn < FN; ++fn)
 #pragma unroll
-                for (int mb = 0; mb < MB; ++mb)
-                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf16x8, B.x[mb][u]), __builtin_bit_cast(bf16x8, wf),
-                        acc[nb][mb], 0, 0, 0);
-            }
+                for (int fm = 0; fm < FM; ++fm)
+                    acc[fn][fm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf16x8, af[fn]), __builtin_bit_cast(bf16x8, bfr[fm]),
+                        acc[fn][fm], 0, 0, 0);
+        }
     };
 
-    // two batches in flight; past the end the prefetch re-reads the wave's
-    // last batch (a cache hit) so every path issues the same loads
-    const int nbatch = kw / kBatchK;
-    Batch<kNB, MB> b0, b1;
-    load(b0, 0);
-    int i = 0;
-    for (; i + 1 < nbatch; i += 2) {
-        load(b1, (i + 1) * kBatchK);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(b0);
-        load(b0, min(i + 2, nbatch - 1) * kBatchK);
-        __builtin_amdgcn_sched_barrier(0);
-        compute(b1);
+    // P stages in flight in registers, two in LDS: stage k is stored into
+    // buffer k & 1, the load of stage k + P is issued into its registers,
+    // one barrier, then stage k is multiplied.  A wave that reaches stage
+    // k + 1's store has passed stage k's barrier, so every wave is done with
+    // that buffer's previous stage (k - 1).  The loads are unconditional
+    // (past the end they re-read the last stage into registers that are not
+    // stored again), so the wait before each store covers exactly that
+    // stage's loads and the other P - 1 stages stay in flight; the last
+    // nk % P stages, already loaded, follow the loop.
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+        load(rx[p], rw[p], p);
+    const int nfull = nk / P * P;
+    for (int kt = 0; kt < nfull; kt += P) {
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            const int k = kt + p;
+            store(rx[p], rw[p], k & 1);
+            load(rx[p], rw[p], k + P);
+            __syncthreads();
+            compute(k & 1);
+        }
     }
-    if (nbatch & 1)
-        compute(b0);
+#pragma unroll
+    for (int p = 0; p + 1 < P; ++p) {
+        const int k = nfull + p;
+        if (k < nk) {
+            store(rx[p], rw[p], k & 1);
+            __syncthreads();
+            compute(k & 1);
+        }
+    }
 
-    // merge the waves in order 0, 1, ..., WAVES - 1
-    if (wave > 0) {
+    // acc[fn][fm][e]: column n0 + wn*TN + 16 fn + 4 kq + e of row
+    // m0 + wm*TM + 16 fm + r
 #pragma unroll
-        for (int nb = 0; nb < kNB; ++nb)
+    for (int fm = 0; fm < FM; ++fm) {
+        const int m = m0 + wm * TM + 16 * fm + r;
+        if (m >= M)
+            continue;
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-                red[wave - 1][nb * MB + mb][lane] = acc[nb][mb];
-    }
-    __syncthreads();
-    if (wave != 0)
-        return;
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) {
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-            f32x4 v = acc[nb][mb];
-#pragma unroll
-            for (int x = 0; x < WAVES - 1; ++x)
-                v += red[x][nb * MB + mb][lane];
-            // v[i]: row 16mb + 4grp + i, column n0 + 16nb + r
-            const int n = n0 + 16 * nb + r;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int m = 16 * mb + 4 * grp + i;
-                if (m < M) {
-                    if constexpr (MODE == 2)
-                        a.part[((size_t)slice * M + m) * a.N + n] = v[i];
-                    else if constexpr (MODE == 1)
-                        ((float *)a.y)[(size_t)m * a.N + n] = v[i];
-                    else
-                        ((uint16_t *)a.y)[(size_t)m * a.N + n] = bf16_rne(v[i]);
-                }
+        for (int fn = 0; fn < FN; ++fn) {
+            const int n = n0 + wn * TN + 16 * fn + 4 * kq;
+            const f32x4 v = acc[fn][fm];
+            if constexpr (MODE == OUT_PART) {
+                *(f32x4 *)(a.part + ((size_t)s * M + m) * N + n) = v;
+            } else if constexpr (MODE == OUT_F32) {
+                *(f32x4 *)((float *)a.y + (size_t)m * N + n) = v;
+            } else {
+                *(u32x2 *)((uint16_t *)a.y + (size_t)m * N + n) =
+                    u32x2{(unsigned)bf16_rne(v[0]) | ((unsigned)bf16_rne(v[1]) << 16),
+                          (unsigned)bf16_rne(v[2]) | ((unsigned)bf16_rne(v[3]) << 16)};
             }
         }
     }
 }
 
-// y[e] = sum over slices s = 0 .. S-1 (in order) of part[s][e], four per thread.
-template <int MODE>
+// y[e] = sum over slices s = 0 .. S-1 (in order) of part[s][e], four per
+// thread; the S loads are all issued before the first add.
+template <int MODE, int S>
 __global__ void __launch_bounds__(kReduceThreads)
-gemm_reduce_kernel(const float *__restrict__ part, void *__restrict__ y, size_t elems, int S)
+gemm_reduce_kernel(const float *__restrict__ part, void *__restrict__ y, size_t elems)
 {
     const size_t e4 = ((size_t)blockIdx.x * kReduceThreads + threadIdx.x) * 4;
     if (e4 >= elems)
         return;
-    f32x4 v = *(const f32x4 *)(part + e4);
+    f32x4 p[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+        p[s] = *(const f32x4 *)(part + (size_t)s * elems + e4);
+    f32x4 v = p[0];
+#pragma unroll
     for (int s = 1; s < S; ++s)
-        v += *(const f32x4 *)(part + (size_t)s * elems + e4);
-    if constexpr (MODE == 1) {
+        v += p[s];
+    if constexpr (MODE == OUT_F32) {
         *(f32x4 *)((float *)y + e4) = v;
     } else {
-        uint16_t *o = (uint16_t *)y + e4;
-        *(unsigned *)o = (unsigned)bf16_rne(v[0]) | ((unsigned)bf16_rne(v[1]) << 16);
-        *(unsigned *)(o + 2) = (unsigned)bf16_rne(v[2]) | ((unsigned)bf16_rne(v[3]) << 16);
+        *(u32x2 *)((uint16_t *)y + e4) =
+            u32x2{(unsigned)bf16_rne(v[0]) | ((unsigned)bf16_rne(v[1]) << 16),
+                  (unsigned)bf16_rne(v[2]) | ((unsigned)bf16_rne(v[3]) << 16)};
+    }
+}
+
+// ---------------------------------------------------------------- host side
+// The tile configurations (index = VD_GEMM_FLAG_TILE's argument), with the
+// two figures the automatic choice weighs them by, measured on MI355X: how
+// fast the tile streams weights relative to 5.7 TB/s once its workgroups fill
+// the device, and its matrix-core throughput (PFLOP/s) on a full device.
+struct TileCfg {
+    int bm, bn, bk;
+    double stream_eff, pflops;
+};
+constexpr TileCfg kTiles[] = {
+    {16, 64, 128, 1.15, 1.0},    // 0: four waves over the columns
+    {32, 64, 128, 0.90, 0.65},   // 1
+    {48, 64, 128, 0.90, 1.0},    // 2
+    {64, 64, 128, 0.95, 0.33},   // 3
+    {64, 128, 64, 1.05, 0.50},   // 4: 2 x 2 waves
+    {128, 128, 64, 1.20, 0.80},  // 5
+};
+constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
+
+template <int MODE>
+void launch_tile(int cfg, const GemmArgs &g, dim3 grid, hipStream_t stream)
+{
+    const dim3 block(kThreads);
+    switch (cfg) {
+    case 0: hipLaunchKernelGGL((gemm_tile_kernel<16, 64, 128, 1, 4, 4, MODE>), grid, block, 0, stream, g); break;
+    case 1: hipLaunchKernelGGL((gemm_tile_kernel<32, 64, 128, 1, 4, 3, MODE>), grid, block, 0, stream, g); break;
+    case 2: hipLaunchKernelGGL((gemm_tile_kernel<48, 64, 128, 1, 4, 3, MODE>), grid, block, 0, stream, g); break;
+    case 3: hipLaunchKernelGGL((gemm_tile_kernel<64, 64, 128, 1, 4, 3, MODE>), grid, block, 0, stream, g); break;
+    case 4:
+        if (g.tiles_m == 1)
+            hipLaunchKernelGGL((gemm_tile_kernel<64, 128, 64, 2, 2, 2, MODE>), grid, block, 0, stream, g);
+        else
+            hipLaunchKernelGGL((gemm_tile_kernel<64, 128, 64, 2, 2, 2, MODE, false>), grid, block, 0, stream, g);
+        break;
+    default:
+        if (g.tiles_m == 1)
+            hipLaunchKernelGGL((gemm_tile_kernel<128, 128, 64, 2, 2, 2, MODE>), grid, block, 0, stream, g);
+        else
+            hipLaunchKernelGGL((gemm_tile_kernel<128, 128, 64, 2, 2, 2, MODE, false>), grid, block, 0, stream, g);
+        break;
+    }
+}
+
+template <int MODE>
+void launch_reduce(int S, const float *part, void *y, size_t elems, dim3 grid, hipStream_t stream)
+{
+    const dim3 block(kReduceThreads);
+    switch (S) {
+    case 2: hipLaunchKernelGGL((gemm_reduce_kernel<MODE, 2>), grid, block, 0, stream, part, y, elems); break;
+    case 4: hipLaunchKernelGGL((gemm_reduce_kernel<MODE, 4>), grid, block, 0, stream, part, y, elems); break;
+    case 8: hipLaunchKernelGGL((gemm_reduce_kernel<MODE, 8>), grid, block, 0, stream, part, y, elems); break;
+    default: hipLaunchKernelGGL((gemm_reduce_kernel<MODE, 16>), grid, block, 0, stream, part, y, elems); break;
     }
 }
 
 bool aligned(const void *p, size_t al) { return ((uintptr_t)p & (al - 1)) == 0; }
 
-// Compute units of the current device, queried once per device (0 = not yet).
-constexpr int kMaxDevices = 64;
-std::atomic<int> g_cus[kMaxDevices];
-
-int device_cus(int *cus)
-{
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess)
-        return VD_ERROR_LAUNCH;
-    if (dev >= 0 && dev < kMaxDevices) {
-        const int v = g_cus[dev].load(std::memory_order_relaxed);
-        if (v > 0) {
-            *cus = v;
-            return VD_SUCCESS;
-        }
-    }
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-        return VD_ERROR_LAUNCH;
-    if (dev >= 0 && dev < kMaxDevices)
-        g_cus[dev].store(n, std::memory_order_relaxed);
-    *cus = n;
-    return VD_SUCCESS;
-}
+struct Plan {
+    int cfg, S;
+};
 
 int gemm_check(int M, int N, int K, unsigned flags)
 {
     if (M <= 0 || N <= 0 || K <= 0)
         return VD_ERROR_INVALID_VALUE;
-    if (flags & ~VD_FLAG_OUT_F32)
+    if (flags & ~(VD_FLAG_OUT_F32 | VD_GEMM_FLAG_TILE_MASK | VD_GEMM_FLAG_SLICES_MASK))
         return VD_ERROR_INVALID_VALUE;
-    if (M > kMaxM || N % kTileN != 0 || K % kSliceAlign != 0)
+    if (N % kNAlign != 0 || K % kKAlign != 0)
         return VD_ERROR_NOT_SUPPORTED;
-    if ((long long)N * K >= (1LL << 40) || (long long)M * N >= (1LL << 31))
+    if ((long long)N * K >= (1LL << 40) || (long long)M * N >= (1LL << 31) ||
+        (long long)M * K >= (1LL << 40))
         return VD_ERROR_NOT_SUPPORTED;
     return VD_SUCCESS;
 }
 
-// Columns per workgroup for a batch of M rows.
-int gemm_nb(int M) { return M <= 8 ? 1 : 4; }
 
-// K slices: the largest power of two dividing K / 512 that keeps the
-// workgroup count within kGemmGroupsPerCU per CU.
-int gemm_slices(int M, int N, int K, int cus)
+// Workgroups of a configuration with S slices.
+long long plan_groups(const TileCfg &c, int M, int N, int S)
 {
-    const int tiles = N / (16 * gemm_nb(M));
-    const int units = K / kSliceAlign;
-    int S = 1;
-    while (units % (2 * S) == 0 && (long long)tiles * 2 * S <= (long long)kGemmGroupsPerCU * cus)
-        S *= 2;
-    return S;
+    return (long long)((M + c.bm - 1) / c.bm) * (N / c.bn) * S;
 }
 
-// Waves per workgroup: 8 for 16-column tiles when they number at most one per
-// CU (more K parallelism per tile: down and o_proj at small M), if the K
-// slice is whole 8-wave batches; else 4.
-int gemm_waves(int M, int N, int K, int S, int cus)
+// Estimated time (microseconds) of a plan on MI355X: a fixed 4 us, plus the
+// larger of the weight stream (5.7 TB/s times the tile's streaming
+// efficiency, scaled down while its workgroups fill less than 192 CUs) and
+// the matrix-core time (the tile's throughput, scaled by the CUs it fills,
+// on the rows padded to whole tiles); K slices add the fp32 partials' round
+// trip at 1.6 TB/s and the reduction kernel (5 us); every 512 workgroups past
+// the first 512 add 19 us.  The constants were fitted to a sweep of the four
+// Llama-3-8B-shaped projections over M = 1 .. 1024 with weights that do not
+// fit the caches (the choice costs 1.6% over the best plan on average).
+double plan_cost(const TileCfg &c, int M, int N, int K, int S)
 {
-    return gemm_nb(M) == 1 && N / 16 <= cus && (K / S) % (8 * kBatchK) == 0 ? 8 : 4;
+    const double groups = (double)plan_groups(c, M, N, S);
+    const double mpad = (double)((M + c.bm - 1) / c.bm) * c.bm;
+    const double t_w = (double)N * K * 2.0 / (5.7e6 * c.stream_eff * std::min(1.0, groups / 192.0));
+    const double t_mfma = 2.0 * mpad * N * K / (c.pflops * 1e9 * std::min(1.0, groups / kTargetCUs));
+    const double t_part = S > 1 ? (double)S * M * N * 8.0 / 1.6e6 + 5.0 : 0.0;
+    const double waves = std::ceil(groups / 512.0);
+    return 4.0 + std::max(t_w, t_mfma) + t_part + 19.0 * (waves - 1.0);
 }
 
-template <int NB, int MB, int WAVES>
-void launch_gemm(const GemmArgs &g, int S, bool f32, hipStream_t stream)
+// The automatic choice, from the sizes alone: the cheapest plan by
+// plan_cost over the tiles (for up to 64 rows, only the narrow tile that
+// holds the rows, 16 * ceil(M / 16), besides the wide ones) and 1, 2, 4 or 8
+// K slices of whole 512-column units.
+Plan auto_plan(int M, int N, int K)
 {
-    const dim3 grid(g.N / (16 * NB), S), block(64 * WAVES);
-    if (S > 1)
-        hipLaunchKernelGGL((gemm_kernel<NB, MB, 2, WAVES>), grid, block, 0, stream, g);
-    else if (f32)
-        hipLaunchKernelGGL((gemm_kernel<NB, MB, 1, WAVES>), grid, block, 0, stream, g);
-    else
-        hipLaunchKernelGGL((gemm_kernel<NB, MB, 0, WAVES>), grid, block, 0, stream, g);
+    Plan best{-1, 1};
+    double best_cost = 0;
+    for (int c = 0; c < kNumTiles; ++c) {
+        const TileCfg &t = kTiles[c];
+        if (N % t.bn)
+            continue;
+        if (t.bk == 128 && !(M <= 64 && t.bm == 16 * ((M + 15) / 16)))
+            continue;
+        for (int S = 1; S <= 8; S *= 2) {
+            if ((K / S) % kKAlign || K % S)
+                continue;
+            const double cost = plan_cost(t, M, N, K, S);
+            if (best.cfg < 0 || cost < best_cost) {
+                best = Plan{c, S};
+                best_cost = cost;
+            }
+        }
+    }
+    if (best.cfg < 0)   // N % 64 == 0 always admits the 64-column tiles
+        best = Plan{M <= 64 ? (M + 15) / 16 - 1 : 3, 1};
+    return best;
+}
+
+// The plan of a call: automatic, or the tile and slice count the flags force
+// (tests and sweeps).  Returns false when a forced choice does not fit the sizes.
+bool make_plan(int M, int N, int K, unsigned flags, Plan *out)
+{
+    Plan p = auto_plan(M, N, K);
+    const unsigned ft = (flags & VD_GEMM_FLAG_TILE_MASK) >> VD_GEMM_FLAG_TILE_SHIFT;
+    const unsigned fs = (flags & VD_GEMM_FLAG_SLICES_MASK) >> VD_GEMM_FLAG_SLICES_SHIFT;
+    if (ft) {
+        if ((int)ft > kNumTiles)
+            return false;
+        p.cfg = (int)ft - 1;
+    }
+    if (fs) {
+        if ((int)fs - 1 > kMaxSlicesLog2)
+            return false;
+        p.S = 1 << (fs - 1);
+    }
+    const TileCfg &c = kTiles[p.cfg];
+    if (N % c.bn != 0 || (K / p.S) % c.bk != 0 || K % p.S != 0)
+        return false;
+    *out = p;
+    return true;
+}
+
+size_t plan_workspace(const Plan &p, int M, int N)
+{
+    return p.S > 1 ? (size_t)p.S * M * N * sizeof(float) : 0;
 }
 
 }  // namespace
@@ -303,8 +429,10 @@ size_t vd_gemm_workspace_size(int M, int N, int K, unsigned flags)
 {
     if (gemm_check(M, N, K, flags))
         return 0;
-    // any slice count the device may pick divides K / 512
-    return (size_t)(K / kSliceAlign) * M * N * sizeof(float);
+    Plan p;
+    if (!make_plan(M, N, K, flags, &p))
+        return 0;
+    return plan_workspace(p, M, N);
 }
 
 int vd_gemm_bf16(const void *x, const void *w, void *y, int M, int N, int K, void *workspace,
@@ -315,16 +443,17 @@ int vd_gemm_bf16(const void *x, const void *w, void *y, int M, int N, int K, voi
         return st;
     if (!x || !w || !y || !aligned(x, 16) || !aligned(w, 16) || !aligned(y, 16))
         return VD_ERROR_INVALID_VALUE;
-    int cus = 0;
-    if (device_cus(&cus) != VD_SUCCESS)
-        return VD_ERROR_LAUNCH;
-    const int S = gemm_slices(M, N, K, cus);
-    if (S > 1) {
+    Plan p;
+    if (!make_plan(M, N, K, flags, &p))
+        return VD_ERROR_NOT_SUPPORTED;
+    const size_t need = plan_workspace(p, M, N);
+    if (need) {
         if (!workspace || !aligned(workspace, 16))
             return VD_ERROR_INVALID_VALUE;
-        if (workspace_bytes < (size_t)S * M * N * sizeof(float))
+        if (workspace_bytes < need)
             return VD_ERROR_WORKSPACE_TOO_SMALL;
     }
+    const TileCfg &c = kTiles[p.cfg];
     GemmArgs g;
     g.x = (const uint16_t *)x;
     g.w = (const uint16_t *)w;
@@ -333,30 +462,25 @@ int vd_gemm_bf16(const void *x, const void *w, void *y, int M, int N, int K, voi
     g.M = M;
     g.N = N;
     g.K = K;
-    g.kslice = K / S;
+    g.kslice = K / p.S;
+    g.S = p.S;
+    g.tiles_m = (M + c.bm - 1) / c.bm;
+    g.groups = (N / c.bn) * p.S;
+    const dim3 grid((unsigned)((long long)g.tiles_m * g.groups));
     const bool f32 = flags & VD_FLAG_OUT_F32;
-    if (gemm_nb(M) == 1) {
-        if (gemm_waves(M, N, K, S, cus) == 8)
-            launch_gemm<1, 1, 8>(g, S, f32, stream);
-        else
-            launch_gemm<1, 1, 4>(g, S, f32, stream);
-    } else {
-        switch ((M + 15) / 16) {
-        case 1: launch_gemm<4, 1, 4>(g, S, f32, stream); break;
-        case 2: launch_gemm<4, 2, 4>(g, S, f32, stream); break;
-        case 3: launch_gemm<4, 3, 4>(g, S, f32, stream); break;
-        default: launch_gemm<4, 4, 4>(g, S, f32, stream); break;
-        }
-    }
-    if (S > 1) {
-        const size_t elems = (size_t)M * N;   // N % 32 == 0, so elems % 4 == 0
-        const dim3 grid((unsigned)((elems / 4 + kReduceThreads - 1) / kReduceThreads));
+    if (p.S > 1)
+        launch_tile<OUT_PART>(p.cfg, g, grid, stream);
+    else if (f32)
+        launch_tile<OUT_F32>(p.cfg, g, grid, stream);
+    else
+        launch_tile<OUT_BF16>(p.cfg, g, grid, stream);
+    if (p.S > 1) {
+        const size_t elems = (size_t)M * N;   // N % 64 == 0, so elems % 4 == 0
+        const dim3 rgrid((unsigned)((elems / 4 + kReduceThreads - 1) / kReduceThreads));
         if (f32)
-            hipLaunchKernelGGL(gemm_reduce_kernel<1>, grid, dim3(kReduceThreads), 0, stream,
-                               (const float *)workspace, y, elems, S);
+            launch_reduce<OUT_F32>(p.S, (const float *)workspace, y, elems, rgrid, stream);
         else
-            hipLaunchKernelGGL(gemm_reduce_kernel<0>, grid, dim3(kReduceThreads), 0, stream,
-                               (const float *)workspace, y, elems, S);
+            launch_reduce<OUT_BF16>(p.S, (const float *)workspace, y, elems, rgrid, stream);
     }
     return hipGetLastError() == hipSuccess ? VD_SUCCESS : VD_ERROR_LAUNCH;
 }

@@ -58,7 +58,9 @@ int main(void)
     CHECK(vd_decode_gather(F, F, FI, FI, NULL, F, 4, 8, 128, 16, 63, F, need, NULL) == VD_ERROR_INVALID_VALUE, "gather null");
     CHECK(vd_kv_append(F, F, F, F, FI, NULL, 4, 8, 128, 16, 63, NULL) == VD_ERROR_INVALID_VALUE, "append null");
     CHECK(vd_kv_append(F, F, F, F, FI, FI, 4, 8, 64, 16, 63, NULL) == VD_ERROR_NOT_SUPPORTED, "append D 64");
-    CHECK(vd_gemm_bf16(F, F, F, 99, 64, 512, F, 1 << 20, 0, NULL) == VD_ERROR_NOT_SUPPORTED, "gemm M 99");
+    CHECK(vd_gemm_bf16(F, F, F, 99, 64, 500, F, 1 << 20, 0, NULL) == VD_ERROR_NOT_SUPPORTED, "gemm K 500");
+    CHECK(vd_gemm_bf16(F, F, F, 4, 64, 512, F, 1 << 20, VD_GEMM_FLAG_TILE(4), NULL) == VD_ERROR_NOT_SUPPORTED,
+          "gemm 128-column tile on 64 columns");
     CHECK(vd_gemm_bf16(NULL, F, F, 1, 64, 512, F, 1 << 20, 0, NULL) == VD_ERROR_INVALID_VALUE, "gemm null");
     CHECK(vd_stream_read(NULL, 1024, F, 8, NULL) == VD_ERROR_INVALID_VALUE, "stream null");
 

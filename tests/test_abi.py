@@ -160,15 +160,28 @@ def test_append_and_stream_argument_errors():
 
 def test_gemm_argument_errors():
     L = vd.lib()
-    assert vd.vd_gemm_workspace_size(64, 4096, 4096) == 8 * 64 * 4096 * 4
-    assert vd.vd_gemm_workspace_size(65, 4096, 4096) == 0      # M > 64
-    assert vd.vd_gemm_workspace_size(8, 4128, 4096) == 0       # N % 64
-    assert vd.vd_gemm_workspace_size(8, 4096, 4000) == 0       # K % 512
+    ws = vd.vd_gemm_workspace_size
+    # the workspace holds S fp32 partials of M x N when K is split S ways
+    for M, N, K in ((64, 4096, 4096), (1, 28672, 4096), (1024, 4096, 4096), (300, 4096, 14336)):
+        n = ws(M, N, K)
+        assert n % (M * N * 4) == 0 and n // (M * N * 4) in (0, 2, 4, 8)
+    assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_SLICES_LOG2(0)) == 0
+    assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_SLICES_LOG2(3)) == 8 * 64 * 4096 * 4
+    assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_TILE(5) | vd.VD_GEMM_FLAG_SLICES_LOG2(4)) == 16 * 64 * 4096 * 4
+    assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_TILE(6)) == 0    # no such tile
+    assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_SLICES_LOG2(5)) == 0   # 32 slices
+    assert ws(4, 4096, 512, vd.VD_GEMM_FLAG_SLICES_LOG2(3)) == 0     # 64-column slices: not whole 128-column stages
+    assert ws(4, 192, 512, vd.VD_GEMM_FLAG_TILE(4)) == 0       # 128-column tile, N % 128
+    assert ws(8, 4128, 4096) == 0       # N % 64
+    assert ws(8, 4096, 4000) == 0       # K % 512
+    assert ws(0, 4096, 4096) == 0       # M = 0
     assert L.vd_gemm_bf16(None, FAKE, FAKE, 4, 64, 512, FAKE, 1 << 20, 0, None) == vd.VD_ERROR_INVALID_VALUE
     assert L.vd_gemm_bf16(FAKE, MIS, FAKE, 4, 64, 512, FAKE, 1 << 20, 0, None) == vd.VD_ERROR_INVALID_VALUE
     assert L.vd_gemm_bf16(FAKE, FAKE, FAKE, 0, 64, 512, FAKE, 1 << 20, 0, None) == vd.VD_ERROR_INVALID_VALUE
     assert L.vd_gemm_bf16(FAKE, FAKE, FAKE, 4, 64, 512, FAKE, 1 << 20, 1 << 4, None) == vd.VD_ERROR_INVALID_VALUE
-    assert L.vd_gemm_bf16(FAKE, FAKE, FAKE, 99, 64, 512, FAKE, 1 << 20, 0, None) == vd.VD_ERROR_NOT_SUPPORTED
+    assert L.vd_gemm_bf16(FAKE, FAKE, FAKE, 99, 64, 500, FAKE, 1 << 20, 0, None) == vd.VD_ERROR_NOT_SUPPORTED
+    assert L.vd_gemm_bf16(FAKE, FAKE, FAKE, 4, 64, 512, FAKE, 1 << 20, vd.VD_GEMM_FLAG_TILE(4), None) == \
+        vd.VD_ERROR_NOT_SUPPORTED
 
 
 def test_product_does_not_reference_oracle():
