@@ -489,6 +489,141 @@ def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
     print(json.dumps({"gemm_points": len(rows)}), flush=True)
 
 
+LAYER_BATCH = (1, 4, 16, 32, 64, 128, 192, 256, 384, 512)
+LAYER_LEN = (16, 64, 256, 1024, 4096)
+LAYER_RING = 4
+
+
+def layer_surface(outdir: str, reps: int = 5):
+    """Time of one decode layer step built from this library's kernels over
+    (N_req, tokens per request): the decode iteration the paper's latency
+    model predicts (Sec. 5.4, Eq. pred-itl), whose N_req term the projection
+    GEMMs carry and whose N_kv term attention carries.  A Llama-3-8B-shaped
+    layer (hidden 4096, 32 query / 8 KV heads of 128, MLP 14336): qkv GEMM,
+    KV append of the new token, decode attention (plan, attention, combine),
+    o_proj, gate_up and down GEMMs.  Norms, rotary embedding and the SiLU
+    product are elementwise work outside this library and are left out; each
+    kernel reads inputs of the right shape, so the timing does not depend on
+    the values.  A ring of four layers, each with its own weights (1.7 GB in
+    all) and its own pages of the KV cache, keeps every step's weights out of
+    the caches, as in a real model whose layers each read theirs once per
+    iteration.  Each point: the four layers captured into one HIP graph
+    (kernel launches only), replayed `reps` times after a warm-up replay and
+    20 ms of untimed replays; per-component graphs of the same four layers
+    give the split.  Fits T = c*N_req + d*N_kv + e and the boosted model."""
+    import numpy as np
+    import torch
+
+    import paper_2509_04827_amd as vd
+    from paper_2509_04827_amd import latency_model as lm
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    gen = torch.Generator(device=dev).manual_seed(0)
+    rng = np.random.default_rng(0)
+    H, Hq, Hkv, D, S, FF = 4096, 32, 8, 128, 16, 14336
+    shapes = {"qkv": (6144, H), "o_proj": (H, H), "gate_up": (2 * FF, H), "down": (H, FF)}
+
+    def rnd(*shape):
+        return torch.randn(shape, generator=gen, device=dev).to(torch.bfloat16)
+
+    weights = [{k: rnd(n, kk) for k, (n, kk) in shapes.items()} for _ in range(LAYER_RING)]
+    max_tok = max(b * l for b in LAYER_BATCH for l in LAYER_LEN)
+    pages_per_layer = max_tok // S + max(LAYER_BATCH)
+    npages = pages_per_layer * LAYER_RING
+    kpool = torch.empty((npages, S, Hkv, D), dtype=torch.bfloat16, device=dev)
+    vpool = torch.empty_like(kpool)
+    for pool in (kpool, vpool):   # filled in slices: no full-size fp32 temporary
+        for i in range(0, npages, 8192):
+            pool[i:i + 8192].copy_(torch.randn(pool[i:i + 8192].shape, generator=gen, device=dev))
+    stream = torch.cuda.current_stream()
+    scale = float(np.float32(1.0 / np.sqrt(D)))
+    rows = []
+
+    for B in LAYER_BATCH:
+        x = rnd(B, H)
+        y_qkv = torch.empty((B, 6144), dtype=torch.bfloat16, device=dev)
+        q = rnd(B, Hq, D)
+        knew, vnew = rnd(B, Hkv, D), rnd(B, Hkv, D)
+        attn_out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=dev)
+        y_o = torch.empty((B, H), dtype=torch.bfloat16, device=dev)
+        y_gu = torch.empty((B, 2 * FF), dtype=torch.bfloat16, device=dev)
+        act = rnd(B, FF)
+        y_down = torch.empty((B, H), dtype=torch.bfloat16, device=dev)
+        gws = {k: torch.empty(max(16, vd.vd_gemm_workspace_size(B, n, kk)), dtype=torch.uint8, device=dev)
+               for k, (n, kk) in shapes.items()}
+        for L in LAYER_LEN:
+            if B * L > max_tok:
+                continue
+            P = (L + S - 1) // S
+            pts, sl = [], torch.full((B,), L, dtype=torch.int32, device=dev)
+            pos = torch.full((B,), L - 1, dtype=torch.int32, device=dev)
+            for layer in range(LAYER_RING):
+                perm = rng.permutation(pages_per_layer)[:B * P] + layer * pages_per_layer
+                pts.append(torch.from_numpy(perm.reshape(B, P).astype(np.int32)).to(dev))
+            aws = vd.alloc_workspace(B, Hq, Hkv, P)
+            # no explicit stream: each call goes to the current stream, the
+            # capture stream while a graph is being recorded
+            comps = {
+                "qkv": lambda w, pt: vd.vd_gemm_bf16(x, w["qkv"], y_qkv, gws["qkv"]),
+                "append": lambda w, pt: vd.vd_kv_append(knew, vnew, kpool, vpool, pt, pos),
+                "attn": lambda w, pt: vd.vd_decode_attn(q, kpool, vpool, pt, sl, attn_out, scale, aws),
+                "o_proj": lambda w, pt: vd.vd_gemm_bf16(attn_out.view(B, H), w["o_proj"], y_o, gws["o_proj"]),
+                "gate_up": lambda w, pt: vd.vd_gemm_bf16(y_o, w["gate_up"], y_gu, gws["gate_up"]),
+                "down": lambda w, pt: vd.vd_gemm_bf16(act, w["down"], y_down, gws["down"]),
+            }
+
+            def graph_us(names):
+                def body():
+                    for layer in range(LAYER_RING):
+                        for n in names:
+                            comps[n](weights[layer], pts[layer])
+                side = torch.cuda.Stream()   # one eager pass first: lazy set-up stays out of the capture
+                side.wait_stream(stream)
+                with torch.cuda.stream(side):
+                    body()
+                stream.wait_stream(side)
+                torch.cuda.synchronize()
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    body()
+                settle_clocks(g.replay, 0.02)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for _ in range(reps):
+                    g.replay()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                del g
+                return e0.elapsed_time(e1) * 1e3 / (reps * LAYER_RING)
+
+            row = dict(n_req=B, tokens_per_req=L, n_kv=B * L)
+            row["us_layer"] = round(graph_us(list(comps)), 2)
+            for n in comps:
+                row["us_" + n] = round(graph_us([n]), 2)
+            rows.append(row)
+            print("layer B %4d L %5d N_kv %8d  layer %8.2f us  (qkv %.1f append %.1f attn %.1f o %.1f gu %.1f down %.1f)"
+                  % (B, L, B * L, row["us_layer"], row["us_qkv"], row["us_append"], row["us_attn"],
+                     row["us_o_proj"], row["us_gate_up"], row["us_down"]), file=sys.stderr, flush=True)
+            del aws, pts
+    os.makedirs(outdir, exist_ok=True)
+    keys = list(rows[0].keys())
+    with open(os.path.join(outdir, "decode_layer_surface.csv"), "w") as f:
+        f.write(",".join(keys) + "\n")
+        for r in rows:
+            f.write(",".join(str(r[k]) for k in keys) + "\n")
+    n_req = np.array([r["n_req"] for r in rows], float)
+    n_kv = np.array([r["n_kv"] for r in rows], float)
+    t = np.array([r["us_layer"] for r in rows], float)
+    fit = lm.fit_linear(n_req, n_kv, t)
+    res = {"points": len(rows), "c_us_per_req": fit.c, "d_us_per_kv_token": fit.d, "e_us": fit.e,
+           "r2": fit.r2, "mae_us": fit.mae, "holdout": lm.holdout_mae(n_req, n_kv, t)}
+    with open(os.path.join(outdir, "decode_layer_surface_fit.json"), "w") as f:
+        json.dump(res, f, indent=1)
+    print(json.dumps(res), flush=True)
+
+
 def next_profile(outdir: str, iters: int = 20, warmup: int = 3):
     """A short, profiler-friendly run of the other kernels: vd_gemm_bf16 on
     the four Llama-3-8B-shaped projections at M = 1, 16, 64, 256, 257 and
@@ -598,6 +733,10 @@ def main():
     ap.add_argument("--cpu-configs", metavar="DIR", default=None,
                     help="time the oracle on the host cores and the GPU on every seeded workload; "
                          "write oracle_cpu_baseline.{csv,json} to DIR")
+    ap.add_argument("--layer-surface", metavar="DIR", default=None,
+                    help="instead of the bench line, time a decode layer step (qkv GEMM, KV append, "
+                         "attention, o_proj / gate_up / down GEMMs) over (batch, tokens per request) "
+                         "and write DIR/decode_layer_surface.csv")
     ap.add_argument("--surface", metavar="DIR", default=None,
                     help="instead of the bench line, measure the latency surface over "
                          "(batch, tokens per request) and write DIR/decode_latency_surface.{csv,md}")
@@ -618,6 +757,9 @@ def main():
 
     if args.surface:
         latency_surface(args.surface)
+        return
+    if args.layer_surface:
+        layer_surface(args.layer_surface)
         return
     if args.gemm_sweep:
         gemm_sweep(args.gemm_sweep)

@@ -9,8 +9,10 @@ the appendix on its XGBoost configuration: absolute-error objective, 1000
 rounds, learning rate 0.1, depth 6, early stopping after 200 rounds).
 
 Here the same two models are fitted to the step times this library's
-decode-attention path measures on MI355X at its fixed clock (the latency
-surface written by ``bench.py --surface``).  CPU only; it consumes the
+kernels measure on MI355X at its fixed clock: the decode-attention surface
+written by ``bench.py --surface``, and the decode layer step (projection
+GEMMs, KV append, attention) written by ``bench.py --layer-surface``, where
+the N_req term is carried by the GEMMs as the paper's model charges it.  CPU only; it consumes the
 measurements and launches nothing.  XGBoost is not available in this
 environment, so the boosted model is scikit-learn's histogram gradient
 boosting with the same objective, rate, depth, round budget and patience

@@ -84,3 +84,36 @@ def test_committed_surface_loads_and_fits():
         assert f.r2 > 0.999
         assert 4000 < f.kv_bandwidth_gbs() < 8000
         assert 0 < f.e < 50
+
+
+def test_committed_layer_surface_charges_requests_to_the_gemms():
+    """The measured decode layer step (qkv / o_proj / gate_up / down GEMMs,
+    KV append, attention) under profiles/: Eq. pred-itl fits it, and the
+    N_req term is material there, carried by the GEMMs (the attention-only
+    surface has c near zero), while the N_kv term stays attention's K/V
+    read rate."""
+    import csv
+    import os
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "profiles", "decode_layer_surface.csv")
+    n_req, n_kv, t = lm.load_surface(path, n_q_heads=None, column="us_layer")
+    assert len(t) >= 40 and (t > 0).all()
+    f = lm.fit_linear(n_req, n_kv, t)
+    assert f.r2 > 0.99
+    # c * N_req at 256 requests is at least a fifth of the step at that
+    # batch and its median length
+    sel = n_req == 256
+    assert f.c > 0 and f.c * 256 > 0.2 * np.median(t[sel])
+    assert 4000 < f.kv_bandwidth_gbs() < 8000
+    # the split: the GEMMs carry c, attention carries d
+    rows = list(csv.DictReader(open(path)))
+    gemm = np.array([sum(float(r[k]) for k in ("us_qkv", "us_o_proj", "us_gate_up", "us_down")) for r in rows])
+    attn = np.array([float(r["us_attn"]) for r in rows])
+    fg = lm.fit_linear(n_req, n_kv, gemm)
+    fa = lm.fit_linear(n_req, n_kv, attn)
+    assert fg.c > 0.8 * f.c and abs(fa.c) < 0.05 * f.c
+    assert fa.d > 0.9 * f.d and abs(fg.d) < 0.1 * f.d
+    # the layer is the sum of its parts, within what replaying the graphs
+    # one component at a time adds in gaps
+    parts = gemm + attn + np.array([float(r["us_append"]) for r in rows])
+    assert np.all(np.abs(parts - t) < 0.15 * t + 10)
