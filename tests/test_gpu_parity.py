@@ -465,6 +465,77 @@ def test_step_record():
         check_f32(out, ref_of(c), "step record run")
 
 
+def test_largest_surface_point_sampled():
+    """The largest point of the latency surface: 512 requests of 16384 tokens
+    (8.4 M tokens, 34 GB of K/V), drawn on the device.  32 sampled (request,
+    query head) rows against the oracle's row function, which reads only
+    those requests' pages (copied to the host as a compact pool with its own
+    page table)."""
+    from workloads import make_device_case
+    B, L = 512, 16384
+    say("case: largest surface point, %d requests x %d tokens (sampled)" % (B, L))
+    d = make_device_case(B, L, 32, 8, seed=31, device=DEV)
+    out = torch.full(d["q"].shape, float("nan"), dtype=torch.float32, device=DEV)
+    ws = vd.alloc_workspace(B, 32, 8, d["max_pages_per_seq"])
+    vd.vd_decode_attn(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"], out,
+                      d["scale"], ws)
+    torch.cuda.synchronize()
+    reqs = [0, 37, 101, 255, 256, 390, 477, 511]
+    heads = [0, 5, 18, 31]
+    pt = d["page_table"][reqs]                                   # [8][P], device
+    P = pt.shape[1]
+    kc = bits(d["k_pages"][pt.reshape(-1).long()].cpu())         # compact pools
+    vc = bits(d["v_pages"][pt.reshape(-1).long()].cpu())
+    ptc = np.arange(len(reqs) * P, dtype=np.int32).reshape(len(reqs), P)
+    sel_b = np.repeat(np.arange(len(reqs)), len(heads)).astype(np.int32)
+    sel_h = np.tile(heads, len(reqs)).astype(np.int32)
+    ref = oracle.decode_attn_rows(bits(d["q"][reqs].cpu()), kc, vc, ptc,
+                                  np.full(len(reqs), L, dtype=np.int32), d["scale"], sel_b, sel_h)
+    got = out[reqs][:, heads].reshape(-1, 128).double().cpu().numpy()
+    check_f32(got, ref, "largest surface point, sampled rows", canary=True)
+    del d, out, ws
+    torch.cuda.empty_cache()
+
+
+def test_step_record_clock_after_settle():
+    """After the power manager has brought the shader clock up (tens of ms of
+    steady work), the stamped clock is a real shader clock: within 1000-2600
+    MHz (MI355X peaks at 2400 MHz; its manager moves it between ~1.4 and
+    2.4 GHz under load).  A stamp that read the wrong counter (e.g. the
+    100 MHz real-time counter twice) would fail.  The first workgroup lives
+    for most of the launch: all workgroups are resident from the start and
+    take equal shares of the tiles."""
+    say("case: step record after clock settle")
+    c = custom([2048] * 64, seed=24, fill="zero")
+    d = dev_case(c)
+    ws = vd.alloc_workspace(64, 32, 8, c["max_pages_per_seq"])
+    out = torch.empty(d["q"].shape, dtype=torch.bfloat16, device=DEV)
+
+    def launch():
+        vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
+                             out, d["scale"], ws, flags=vd.VD_FLAG_SELF_PLAN)
+
+    import time
+    t_end = time.time() + 0.1
+    while time.time() < t_end:
+        for _ in range(20):
+            launch()
+        torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(20):
+        launch()
+    e1.record()
+    torch.cuda.synchronize()
+    us_kernel = e0.elapsed_time(e1) * 1e3 / 20
+    n, t0, c0, t1, c1 = _step_record(ws)     # the last launch's record
+    us_first = (t1 - t0) * 0.01
+    mhz = (c1 - c0) * 100.0 / max(t1 - t0, 1)
+    say("  first group %.1f us of %.1f us per launch, shader clock %.0f MHz" % (us_first, us_kernel, mhz))
+    assert 1000.0 <= mhz <= 2600.0
+    assert 0.6 * us_kernel <= us_first <= 1.05 * us_kernel
+
+
 @pytest.mark.parametrize("trial", range(8))
 def test_staged_equals_whole_random(trial):
     """Seeded random shapes, with request counts past one per planning thread

@@ -93,3 +93,20 @@ def test_pins_reject_mutant(tmp_path, oracle_lib, name):
         except (AssertionError, RuntimeError, IndexError, ValueError):
             failed.append(pin.__name__)
     assert failed, "no pin rejects mutant %s" % name
+
+
+def test_rows_function_equals_full_oracle(oracle_lib):
+    """The oracle's sampled-row function (used where the full output is too
+    slow on the CPU) returns exactly the full oracle's rows: same arithmetic,
+    same order, bit for bit."""
+    import numpy as np
+    from workloads import Workload, bits, make_case
+    w = Workload("custom", 5, 32, 8, 128, 16, "fixed", (1, 17, 300, 0, 1000))
+    c = make_case(w, seed=8, fill="nan")
+    args = (bits(c["q"]), bits(c["k_pages"]), bits(c["v_pages"]), c["page_table"].numpy(),
+            c["seq_lens"].numpy())
+    full = oracle_lib.decode_attn(*args, c["scale"])
+    sel_b = np.array([0, 1, 2, 2, 3, 4, 4], dtype=np.int32)
+    sel_h = np.array([0, 31, 5, 6, 9, 0, 31], dtype=np.int32)
+    rows = oracle_lib.decode_attn_rows(*args, c["scale"], sel_b, sel_h)
+    assert np.array_equal(rows, full[sel_b, sel_h])

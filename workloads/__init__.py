@@ -205,3 +205,29 @@ def bits(t: torch.Tensor) -> np.ndarray:
 def kv_bytes(case: dict) -> int:
     """Bytes of K and V a decode step must read: N_kv * Hkv * D * 2 (K,V) * 2 B."""
     return case["n_kv"] * case["n_kv_heads"] * case["head_dim"] * 2 * 2
+
+
+def make_device_case(num_seqs: int, seq_len: int, n_q_heads: int, n_kv_heads: int, seed: int,
+                     device="cuda") -> dict:
+    """A large seeded case drawn directly in device memory (for sizes whose
+    host copy would be tens of GB): every request holds seq_len tokens,
+    pages are a random permutation of the pool, Q/K/V are N(0, 1) rounded to
+    bf16 (torch's generator on `device`, seeded).  Tests check it on sampled
+    rows, copying only the pages those rows read to the host."""
+    gen = torch.Generator(device=device).manual_seed(seed)
+    S, D = 16, 128
+    P = (seq_len + S - 1) // S
+    n_pages = num_seqs * P
+    perm = torch.randperm(n_pages, generator=gen, device=device).to(torch.int32)
+    pools = []
+    for _ in range(2):
+        pool = torch.empty((n_pages, S, n_kv_heads, D), dtype=torch.bfloat16, device=device)
+        for i in range(0, n_pages, 4096):   # no full-size fp32 temporary
+            j = min(n_pages, i + 4096)
+            pool[i:j].copy_(torch.randn((j - i, S, n_kv_heads, D), generator=gen, device=device))
+        pools.append(pool)
+    q = torch.randn((num_seqs, n_q_heads, D), generator=gen, device=device).to(torch.bfloat16)
+    return {"q": q, "k_pages": pools[0], "v_pages": pools[1], "page_table": perm.view(num_seqs, P),
+            "seq_lens": torch.full((num_seqs,), seq_len, dtype=torch.int32, device=device),
+            "num_seqs": num_seqs, "n_q_heads": n_q_heads, "n_kv_heads": n_kv_heads,
+            "max_pages_per_seq": P, "scale": float(np.float32(1.0 / np.sqrt(D)))}
