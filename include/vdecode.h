@@ -128,10 +128,14 @@ size_t vd_decode_workspace_size(int num_seqs, int n_q_heads, int n_kv_heads,
                                 int max_pages_per_seq, unsigned flags);
 
 /*
- * The whole decode-attention step, two kernels enqueued on `stream`: the
- * attention kernel, planning the step itself (vd_decode_partial with
- * VD_FLAG_SELF_PLAN), then the combine kernel (vd_decode_combine).  The
- * result equals that of the staged calls bit for bit.
+ * The whole decode-attention step, enqueued on `stream`: the attention
+ * kernel, planning the step itself (vd_decode_partial with
+ * VD_FLAG_SELF_PLAN), then the combine kernel (vd_decode_combine).  Tiny
+ * steps (every request at most 4 pages, and at most a quarter as many
+ * (page, KV-head group) tiles as the device runs attention workgroups at
+ * once) are cut into whole requests, leave nothing to merge, and run the
+ * attention kernel alone.  The result equals that of the staged calls bit
+ * for bit.
  * scale: the softmax scale applied to q.k (1/sqrt(head_dim) for standard
  * attention); must be finite.
  */

@@ -26,7 +26,9 @@
 // index in the group.
 //
 // Kernels on the caller's stream.  The whole step (vd_decode_attn) is two:
-// a self-planned attention kernel and the combine kernel.  The staged API
+// a self-planned attention kernel and the combine kernel (the attention
+// kernel alone for tiny steps, whose short plan cuts no segment; see
+// short_plan).  The staged API
 // runs the planner first, once per step, and a planned attention kernel per
 // layer.
 //   plan_kernel     one workgroup: tile offsets per request, range starts,
@@ -86,6 +88,9 @@ constexpr int kDeferEntries = 64;      // LDS result entries per wave, over G qu
 constexpr int kPrePad = 6;             // self-planned prefix in LDS: one pad word per 64 entries
 constexpr int kAttnMaxThreads = 64 * kHeadsPerGroup;
 constexpr int kCombineThreads = 512;
+// Short plans (see short_plan): every request at most this many pages, and
+// all requests' tiles together at most a quarter of the resident workgroups.
+constexpr int kShortMaxPages = 4;
 constexpr int kCombineGroupsPerCU = 2;
 constexpr float kLog2e = 1.4426950408889634f;
 // Lazy rescaling: the running max is only raised when a new score exceeds it
@@ -174,14 +179,33 @@ __device__ inline int clamped_len(const int32_t *seq_lens, int b, int maxp)
 // arithmetic keeps the divisions short.)
 __device__ inline unsigned ceil_div_u(unsigned a, unsigned b) { return (a + b - 1) / b; }
 
-__device__ inline int plan_ranges(int T, int forced, int R)
+__device__ inline int plan_ranges(int T, int forced, int R, bool shrt)
 {
     if (T == 0)
         return 0;
     const unsigned t = (unsigned)T;
     if (forced > 0)
         return (int)ceil_div_u(t, (unsigned)forced);
+    if (shrt)   // at most one range per workgroup
+        return T < R ? T : R;
     return T < R ? T : (int)((unsigned)R * ceil_div_u(t, (unsigned)kMaxRangeTiles * R));
+}
+
+// A short plan cuts no (request, head group) segment: each range starts at
+// the first segment that begins at or after its equal-length start, so every
+// piece is a whole segment, writes the final output, and nothing is left to
+// merge.  It is chosen from the sizes alone (every request at most
+// max_pages_per_seq pages), so the host knows that no combine kernel is
+// needed: for tiny steps, every request at most kShortMaxPages pages and at
+// most R / 4 (page, head group) tiles in all.  There a wave's chain of at
+// most four pages costs less than the combine launch it saves (interleaved
+// A/B on MI355X: 8-21% faster steps at 1-32 requests of 16-64 tokens); on
+// larger steps the split plan's balance wins (2-4% at 64-512 requests of
+// 16-64 tokens, and more on ragged mixes of longer requests).
+__host__ __device__ inline bool short_plan(int B, int Hg, int maxp, int R, int forced)
+{
+    return forced <= 0 && maxp <= kShortMaxPages &&
+           4LL * B * Hg * maxp <= (long long)R;
 }
 
 // first tile of range w: floor(w * T / W)
@@ -237,6 +261,27 @@ __device__ inline int find_request(const int *pre, int B, int t)
     return lo;
 }
 
+// First tile of range w of a short plan: the start of the first segment that
+// begins at or after floor(w * T / W); T for w = W.  A range may be empty.
+template <int PAD>
+__device__ inline int short_start(const int *pre, int B, int Hg, int w, int T, int W)
+{
+    if (w >= W)
+        return T;
+    const int t = range_start(w, T, W);   // < T
+    const int b = find_request<PAD>(pre, B, t);
+    const int P = (pre[pidx<PAD>(b + 1)] - pre[pidx<PAD>(b)]) / Hg;   // > 0: tile t lies in b
+    const int off = t - pre[pidx<PAD>(b)];
+    return pre[pidx<PAD>(b)] + (off + P - 1) / P * P;
+}
+
+// First tile of range w under either plan.
+template <int PAD>
+__device__ inline int plan_start(const int *pre, int B, int Hg, int w, int T, int W, bool shrt)
+{
+    return shrt ? short_start<PAD>(pre, B, Hg, w, T, W) : range_start(w, T, W);
+}
+
 // Descriptor {b, q, j, t} of range w, whose first tile t lies in request b,
 // and its boundary record.
 template <int PAD>
@@ -250,12 +295,18 @@ __device__ inline void entry_at(const int *pre, int b, int Hg, int w, int t, int
     rec = boundary_record(w, t, b * Hg + q, j, P, T, W);
 }
 
-// The same for any range: the request found by binary search.
+// The same for range w starting at tile t: the request found by binary
+// search.  A range starting at T (an empty last range of a short plan) gets
+// the end sentinel and an empty record.
 template <int PAD>
-__device__ inline void range_entry(const int *pre, int B, int Hg, int w, int T, int W, int4 &desc,
-                                   int4 &rec)
+__device__ inline void range_entry(const int *pre, int B, int Hg, int w, int t, int T, int W,
+                                   int4 &desc, int4 &rec)
 {
-    const int t = range_start(w, T, W);
+    if (t >= T) {
+        desc = make_int4(B, 0, 0, T);
+        rec = make_int4(0, 0, 0, 0);
+        return;
+    }
     entry_at<PAD>(pre, find_request<PAD>(pre, B, t), Hg, w, t, T, W, desc, rec);
 }
 
@@ -292,7 +343,7 @@ __device__ inline T wave_inclusive_scan(T x, int lane)
 // scan of the per-wave totals give every request's first tile and token.
 __global__ void __launch_bounds__(kPlanThreads)
 plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int forced,
-            int resident_groups, char *__restrict__ ws, WsLayout lay)
+            int resident_groups, int shrt, char *__restrict__ ws, WsLayout lay)
 {
     __shared__ int s_pre[kMaxSeqs + 1];
     __shared__ int s_wtiles[kPlanThreads / 64];
@@ -352,7 +403,7 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
     }
     __syncthreads();
     const int T = s_pre[B];
-    const int W = plan_ranges(T, forced, resident_groups);
+    const int W = plan_ranges(T, forced, resident_groups, shrt != 0);
 
     // range starts {b, q, j, t} (range W is the end sentinel) and the
     // boundary records of ranges 1 .. W-1
@@ -364,7 +415,8 @@ plan_kernel(const int32_t *__restrict__ seq_lens, int B, int Hg, int maxp, int f
             continue;
         }
         int4 desc, rec;
-        range_entry<0>(s_pre, B, Hg, w, T, W, desc, rec);
+        range_entry<0>(s_pre, B, Hg, w, plan_start<0>(s_pre, B, Hg, w, T, W, shrt != 0), T, W,
+                       desc, rec);
         ranges[w] = desc;
         if (w > 0)
             bounds[w] = rec;
@@ -391,6 +443,9 @@ struct AttnArgs {
     float *part_acc;
     int Hq, Hkv, HW, pt_stride, maxp;
     int B, forced, resident;        // requests, forced range length (self-planned); R = grid size
+    int shrt;                       // short plan (short_plan): no segment is cut
+    int zero_empty;                 // self-planned short plan with no combine kernel after it:
+                                    // the attention kernel writes the empty requests' zeros
     float scale_log2;
 };
 
@@ -574,6 +629,7 @@ struct PieceWalk {
 // own ranges' first tile and their boundary records.  Workgroup 0 also writes
 // the header and the list of requests without tokens for the combine kernel.
 // Returns false when the workgroup has no range.
+template <int MODE>
 __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWalk &walk)
 {
     __shared__ uint2 s_wsum[kHeadsPerGroup];
@@ -633,28 +689,65 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
         s_pre[pidx<kPrePad>(B)] = T;
     __syncthreads();
 
-    const int W = plan_ranges(T, a.forced, a.resident);
+    const bool shrt = a.shrt != 0;
+    const int W = plan_ranges(T, a.forced, a.resident, shrt);
     const int2 wr = group_ranges(blockIdx.x, a.resident, W);
-    if (wr.x < wr.y) {
-        // the first range: its first tile lies among the requests of one
-        // thread, which walks them (no search)
-        const int t0 = range_start(wr.x, T, W);
-        const int my0 = excl_t, my1 = excl_t + (int)my_t;
-        if (my0 <= t0 && t0 < my1) {
-            int b = c0;
-            while (s_pre[pidx<kPrePad>(b + 1)] <= t0)
-                ++b;
+    __shared__ int s_tend;   // short plan: the end of this workgroup's one range
+    if (shrt) {
+        // at most one range per workgroup, found by binary search; its
+        // boundary record is empty (no segment is cut)
+        if (tid == 0 && wr.x < wr.y) {
+            const int t0 = short_start<kPrePad>(s_pre, B, Hg, wr.x, T, W);
+            const int t1 = short_start<kPrePad>(s_pre, B, Hg, wr.x + 1, T, W);
             int4 desc, rec;
-            entry_at<kPrePad>(s_pre, b, Hg, wr.x, t0, T, W, desc, rec);
+            range_entry<kPrePad>(s_pre, B, Hg, wr.x, t0, T, W, desc, rec);
             s_desc = desc;
+            s_tend = t1;
             if (wr.x > 0)
-                a.bounds[wr.x] = rec;
+                a.bounds[wr.x] = make_int4(0, 0, 0, 0);
         }
-    }
-    for (int w = wr.x + 1 + tid; w < wr.y; w += nt) {
-        int4 desc, rec;
-        range_entry<kPrePad>(s_pre, B, Hg, w, T, W, desc, rec);
-        a.bounds[w] = rec;
+        if (a.zero_empty) {
+            // no combine kernel follows: this workgroup writes the zero rows
+            // of the requests without tokens in its share of the requests
+            const int bz0 = (int)((long long)blockIdx.x * B / a.resident);
+            const int bz1 = (int)((long long)(blockIdx.x + 1) * B / a.resident);
+            const int row = a.Hq * kHeadDim;
+            for (int b = bz0; b < bz1; ++b) {
+                if (s_pre[pidx<kPrePad>(b + 1)] != s_pre[pidx<kPrePad>(b)])
+                    continue;
+                if constexpr (MODE == MODE_F32) {
+                    float *o = (float *)a.out + (size_t)b * row;
+                    for (int i = tid; i < row / 4; i += nt)
+                        *(f32x4 *)(o + 4 * i) = f32x4{0.f, 0.f, 0.f, 0.f};
+                } else {
+                    uint16_t *o = (uint16_t *)a.out + (size_t)b * row;
+                    for (int i = tid; i < row / 8; i += nt)
+                        *(u32x4 *)(o + 8 * i) = u32x4{0u, 0u, 0u, 0u};
+                }
+            }
+        }
+    } else {
+        if (wr.x < wr.y) {
+            // the first range: its first tile lies among the requests of one
+            // thread, which walks them (no search)
+            const int t0 = range_start(wr.x, T, W);
+            const int my0 = excl_t, my1 = excl_t + (int)my_t;
+            if (my0 <= t0 && t0 < my1) {
+                int b = c0;
+                while (s_pre[pidx<kPrePad>(b + 1)] <= t0)
+                    ++b;
+                int4 desc, rec;
+                entry_at<kPrePad>(s_pre, b, Hg, wr.x, t0, T, W, desc, rec);
+                s_desc = desc;
+                if (wr.x > 0)
+                    a.bounds[wr.x] = rec;
+            }
+        }
+        for (int w = wr.x + 1 + tid; w < wr.y; w += nt) {
+            int4 desc, rec;
+            range_entry<kPrePad>(s_pre, B, Hg, w, range_start(w, T, W), T, W, desc, rec);
+            a.bounds[w] = rec;
+        }
     }
     if (blockIdx.x == 0) {
         // header, and the requests without tokens in order: those before c0
@@ -673,7 +766,10 @@ __device__ inline bool self_plan(const AttnArgs &a, int Hg, int *s_pre, PieceWal
     if (wr.x >= wr.y)
         return false;
     const int4 d = s_desc;
-    walk = PieceWalk{wr.x, wr.y, T, W, d.x, d.y, d.z, d.w, range_start(wr.x + 1, T, W)};
+    const int t_end = shrt ? s_tend : range_start(wr.x + 1, T, W);
+    if (d.w >= t_end)   // an empty range (short plans only)
+        return false;
+    walk = PieceWalk{wr.x, wr.y, T, W, d.x, d.y, d.z, d.w, t_end};
     return true;
 }
 
@@ -909,7 +1005,7 @@ __device__ inline void attn_body(const AttnArgs &a)
     extern __shared__ __attribute__((aligned(16))) char s_dyn[];
     PieceWalk walk;
     if constexpr (SELF) {
-        if (!self_plan(a, Hg, (int *)s_dyn, walk))
+        if (!self_plan<MODE>(a, Hg, (int *)s_dyn, walk))
             return;
     } else {
         const const_i32p hdr = (const const_i32p)a.hdr;
@@ -917,8 +1013,12 @@ __device__ inline void attn_body(const AttnArgs &a)
         const int2 wr = group_ranges(blockIdx.x, a.resident, W);
         if (wr.x >= wr.y)
             return;
+        // the first range's descriptor from the plan; entry wr.x + 1 gives
+        // the tile where that range ends (entry W is the end sentinel)
         const const_i32p rg = (const_i32p)(a.ranges + wr.x);
-        walk = PieceWalk{wr.x, wr.y, T, W, rg[0], rg[1], rg[2], rg[3], range_start(wr.x + 1, T, W)};
+        if (rg[3] >= rg[7])   // an empty range (short plans only)
+            return;
+        walk = PieceWalk{wr.x, wr.y, T, W, rg[0], rg[1], rg[2], rg[3], rg[7]};
     }
     Piece cur;
     if (!walk.next(a, Hg, cur))
@@ -1440,8 +1540,10 @@ int enqueue_plan(const int32_t *seq_lens, int num_seqs, int G, int n_kv_heads,
     if (st)
         return st;
     const WsLayout lay = ws_layout(num_seqs, G, n_kv_heads, max_pages_per_seq, forced_tiles(flags));
+    const int shrt = short_plan(num_seqs, n_kv_heads / HW, max_pages_per_seq, groups,
+                                forced_tiles(flags)) ? 1 : 0;
     hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, seq_lens, num_seqs,
-                       n_kv_heads / HW, max_pages_per_seq, forced_tiles(flags), groups,
+                       n_kv_heads / HW, max_pages_per_seq, forced_tiles(flags), groups, shrt,
                        (char *)workspace, lay);
     return launch_status();
 }
@@ -1457,6 +1559,8 @@ int enqueue_attn(const AttnArgs &args, int G, int mode, bool self, hipStream_t s
         return VD_ERROR_NOT_SUPPORTED;
     AttnArgs copy = args;
     copy.resident = groups;
+    copy.shrt = short_plan(args.B, args.Hkv / args.HW, args.maxp, groups, args.forced) ? 1 : 0;
+    copy.zero_empty = copy.shrt && args.zero_empty;
     void *params[] = {(void *)&copy};
     if (hipLaunchKernel(k, dim3(groups), dim3(64 * args.HW), params,
                         attn_lds_bytes(G, mode, args.HW), stream) != hipSuccess)
@@ -1569,7 +1673,7 @@ int enqueue_partial(const void *q, const void *k_pages, const void *v_pages,
                     const int32_t *page_table, const int32_t *seq_lens, void *out, int num_seqs,
                     int n_q_heads, int n_kv_heads, float scale, int max_pages_per_seq,
                     const WsLayout &lay, void *workspace, unsigned flags, bool self,
-                    hipStream_t stream)
+                    bool zero_empty, hipStream_t stream)
 {
     const int G = n_q_heads / n_kv_heads;
     AttnArgs a = make_args(lay, workspace, num_seqs, n_q_heads, n_kv_heads, max_pages_per_seq,
@@ -1580,7 +1684,31 @@ int enqueue_partial(const void *q, const void *k_pages, const void *v_pages,
     a.pt = page_table;
     a.seq_lens = seq_lens;
     a.out = out;
+    a.zero_empty = zero_empty ? 1 : 0;
     return enqueue_attn(a, G, out_mode(flags), self, stream);
+}
+
+// The whole step: the self-planned attention kernel, then the combine kernel
+// unless the plan is short (no segment cut, so nothing to merge; the
+// attention kernel then writes the empty requests' zeros itself).
+int enqueue_step(const void *q, const void *k_pages, const void *v_pages,
+                 const int32_t *page_table, const int32_t *seq_lens, void *out, int num_seqs,
+                 int n_q_heads, int n_kv_heads, float scale, int max_pages_per_seq,
+                 const WsLayout &lay, void *workspace, unsigned flags, hipStream_t stream)
+{
+    const int G = n_q_heads / n_kv_heads, HW = heads_per_group(n_kv_heads);
+    int groups = 0;
+    int st = resident_attn_groups(G, out_mode(flags), HW, &groups);
+    if (st)
+        return st;
+    const bool shrt = short_plan(num_seqs, n_kv_heads / HW, max_pages_per_seq, groups,
+                                 forced_tiles(flags));
+    st = enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
+                         n_kv_heads, scale, max_pages_per_seq, lay, workspace, flags, true, shrt,
+                         stream);
+    if (st || shrt)
+        return st;
+    return enqueue_combine(out, num_seqs, n_q_heads, n_kv_heads, lay, workspace, flags, stream);
 }
 
 // ---------------------------------------------------------------- fixed scratch
@@ -1682,7 +1810,7 @@ int vd_decode_partial(const void *q, const void *k_pages, const void *v_pages,
                                    forced_tiles(flags));
     return enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
                            n_kv_heads, scale, max_pages_per_seq, lay, workspace, flags,
-                           (flags & VD_FLAG_SELF_PLAN) != 0, stream);
+                           (flags & VD_FLAG_SELF_PLAN) != 0, false, stream);
 }
 
 int vd_decode_combine(void *out, int num_seqs, int n_q_heads, int n_kv_heads, int head_dim,
@@ -1717,14 +1845,10 @@ int vd_decode_attn(const void *q, const void *k_pages, const void *v_pages,
         return st;
     if (num_seqs == 0)
         return VD_SUCCESS;
-    // self-planned attention, then the combine kernel
     const WsLayout lay = ws_layout(num_seqs, n_q_heads / n_kv_heads, n_kv_heads, max_pages_per_seq,
                                    forced_tiles(flags));
-    st = enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
-                         n_kv_heads, scale, max_pages_per_seq, lay, workspace, flags, true, stream);
-    if (st)
-        return st;
-    return enqueue_combine(out, num_seqs, n_q_heads, n_kv_heads, lay, workspace, flags, stream);
+    return enqueue_step(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
+                        n_kv_heads, scale, max_pages_per_seq, lay, workspace, flags, stream);
 }
 
 int vd_decode_attn_noalloc(const void *q, const void *k_pages, const void *v_pages,
@@ -1755,11 +1879,8 @@ int vd_decode_attn_noalloc(const void *q, const void *k_pages, const void *v_pag
     st = noalloc_scratch(&ws);
     if (st)
         return st;
-    st = enqueue_partial(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
-                         n_kv_heads, scale, max_pages_per_seq, lay, ws, flags, true, stream);
-    if (st)
-        return st;
-    return enqueue_combine(out, num_seqs, n_q_heads, n_kv_heads, lay, ws, flags, stream);
+    return enqueue_step(q, k_pages, v_pages, page_table, seq_lens, out, num_seqs, n_q_heads,
+                        n_kv_heads, scale, max_pages_per_seq, lay, ws, flags, stream);
 }
 
 int vd_decode_gather(const void *k_pages, const void *v_pages, const int32_t *page_table,

@@ -350,6 +350,55 @@ def test_empty_requests():
     assert torch.equal(got, torch.zeros_like(got))
 
 
+@pytest.mark.parametrize("case", ["mixed_le64", "ragged_le16", "one_page_each", "all_empty_short",
+                                  "at_limit"])
+def test_short_plan_steps(case):
+    """Tiny steps (every request at most 4 pages, at most a quarter as many
+    (page, head group) tiles as resident workgroups) take the short plan:
+    ranges start at segment starts, every piece is a whole segment, the whole
+    step runs no combine kernel and the attention kernel writes the empty
+    requests' zeros.  Against the oracle, empty rows exactly zero over
+    NaN-filled output, and bit for bit equal to the staged calls (planner
+    kernel, attention, combine) on the same plan."""
+    rng = np.random.default_rng(77)
+    if case == "mixed_le64":
+        lengths = [0, 5, 0, 64, 0, 17, 1, 33]
+    elif case == "ragged_le16":
+        lengths = [int(x) for x in rng.integers(0, 17, 30)]
+        lengths[7] = 0
+    elif case == "one_page_each":
+        lengths = [16] * 32
+    elif case == "all_empty_short":
+        lengths = [0] * 30
+    else:                             # 8 x 2 x 4 tiles: exactly R / 4 at 256 workgroups
+        lengths = [64, 49, 50, 63, 64, 1, 60, 64]
+    say("case: short plan %s (%d requests, longest %d)" % (case, len(lengths), max(lengths)))
+    c = custom(lengths, seed=78)
+    d = dev_case(c)
+    ref = ref_of(c)
+    for dtype in (torch.float32, torch.bfloat16):
+        whole = run_gpu(d, dtype)
+        empty = [b for b, x in enumerate(lengths) if x == 0]
+        if empty:
+            assert torch.equal(whole[empty], torch.zeros_like(whole[empty]))
+        if dtype is torch.float32:
+            check_f32(whole, ref, "short " + case, canary=True)
+        else:
+            check_bf16(whole, ref, "short " + case)
+        maxp = d["page_table"].shape[1]
+        ws = vd.alloc_workspace(len(lengths), 32, 8, maxp)
+        staged = torch.full(d["q"].shape, float("nan"), dtype=dtype, device=DEV)
+        vd.vd_decode_plan(d["seq_lens"], 32, 8, maxp, ws)
+        vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"], staged,
+                             d["scale"], ws)
+        vd.vd_decode_combine(staged, 8, maxp, ws)
+        torch.cuda.synchronize()
+        view = torch.int32 if dtype is torch.float32 else torch.int16
+        assert torch.equal(staged.view(view), whole.view(view))
+        info = vd.step_info(ws)
+        assert info["n_ranges"] <= 256 and info["n_empty"] == len(empty)
+
+
 def test_large_scores():
     """Scores around 5.8e3: only a max-subtracted softmax survives."""
     say("case: large scores")

@@ -80,6 +80,24 @@ def test_noalloc_forced_ranges_and_empty_requests():
     assert np.abs(g - ref).max() <= GATE_MAX_ABS
 
 
+def test_noalloc_short_plan():
+    """A step of short requests takes the short plan (no combine kernel;
+    the attention kernel writes the empty rows): equal to vd_decode_attn."""
+    torch.cuda.set_device(DEV)
+    from workloads import Workload
+    lens = (0, 12, 64, 3, 0, 40, 16, 1)
+    w = Workload("custom", len(lens), 32, 8, 128, 16, "fixed", lens)
+    c = make_case(w, seed=5, fill="nan")
+    d = _dev(c)
+    say("case: noalloc short plan, lengths %s" % (lens,))
+    got = _run(d, torch.float32, True)
+    base = _run(d, torch.float32, False)
+    assert torch.equal(got.view(torch.int32), base.view(torch.int32))
+    assert torch.equal(got[0], torch.zeros_like(got[0])) and torch.equal(got[4], torch.zeros_like(got[4]))
+    g = got.double().cpu().numpy()
+    assert np.abs(g - _oracle(c)).max() <= GATE_MAX_ABS
+
+
 def test_noalloc_refuses_sizes_beyond_the_scratch():
     torch.cuda.set_device(DEV)
     B, Hq, Hkv = 4000, 32, 8       # ~66 MB of partial slots at one page per request
