@@ -624,6 +624,96 @@ def layer_surface(outdir: str, reps: int = 5):
     print(json.dumps(res), flush=True)
 
 
+def score_ab(outdir: str, workloads, rounds: int = 7, iters: int = 50, flushed: int = 30):
+    """The two score paths of the attention kernel against each other: the
+    matrix-core score (default) and the vector-ALU one (VD_FLAG_SCORE_VALU:
+    bf16 pair dot products summed across lanes by DPP).  Per workload (seed
+    0, the bench's inputs), in one process on the same inputs and clocks:
+    `rounds` rounds that alternate which path goes first, each timing
+    `iters` back-to-back attention launches (the self-planned kernel alone,
+    events around the burst) and `iters` whole steps per path; then
+    `flushed` single launches per path, interleaved, each after a 1 GiB read
+    that flushes the caches.  Medians over rounds / launches.  Writes
+    DIR/attn_score_ab.{csv,json}."""
+    import numpy as np
+    import torch
+
+    import paper_2509_04827_amd as vd
+    from workloads import kv_bytes, make_case
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    V = vd.VD_FLAG_SCORE_VALU
+    paths = (("mfma", 0), ("valu", V))
+    fbuf = torch.zeros(1 << 30, dtype=torch.uint8, device=dev)
+    fsink = torch.zeros(4, dtype=torch.int32, device=dev)
+    rows = []
+    for name in workloads:
+        c = make_case(name, seed=0, fill="zero")
+        q, k, v = c["q"].to(dev), c["k_pages"].to(dev), c["v_pages"].to(dev)
+        pt, sl = c["page_table"].to(dev), c["seq_lens"].to(dev)
+        B, Hq, Hkv, maxp = c["num_seqs"], c["n_q_heads"], c["n_kv_heads"], c["max_pages_per_seq"]
+        out = torch.empty(q.shape, dtype=torch.bfloat16, device=dev)
+        ws = vd.alloc_workspace(B, Hq, Hkv, maxp)
+        nbytes = kv_bytes(c)
+        print("score-ab: %s N_req %d N_kv %d" % (name, B, c["n_kv"]), file=sys.stderr, flush=True)
+
+        def attn(f):
+            vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws,
+                                 flags=vd.VD_FLAG_SELF_PLAN | f, stream=stream)
+
+        def whole(f):
+            vd.vd_decode_attn(q, k, v, pt, sl, out, c["scale"], ws, flags=f, stream=stream)
+
+        def burst(fn, f):
+            for _ in range(3):
+                fn(f)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(iters):
+                fn(f)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) * 1e3 / iters
+
+        settle_clocks(lambda: whole(0), 0.3)
+        t = {p: {"attn": [], "step": [], "flushed": []} for p, _ in paths}
+        for r in range(rounds):
+            for p, f in (paths if r % 2 == 0 else paths[::-1]):
+                t[p]["attn"].append(burst(attn, f))
+                t[p]["step"].append(burst(whole, f))
+        for i in range(flushed):
+            for p, f in (paths if i % 2 == 0 else paths[::-1]):
+                vd.vd_stream_read(fbuf, fsink, stream=stream)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                attn(f)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                t[p]["flushed"].append(e0.elapsed_time(e1) * 1e3)
+        row = {"workload": name, "G": Hq // Hkv, "n_req": B, "n_kv": c["n_kv"], "kv_bytes": nbytes,
+               "rounds": rounds, "iters": iters, "flushed": flushed}
+        for p, _ in paths:
+            for kind in ("attn", "step", "flushed"):
+                row["%s_%s_us" % (p, kind)] = round(float(np.median(t[p][kind])), 2)
+            row["%s_attn_gbs" % p] = round(nbytes / (row["%s_attn_us" % p] * 1e-6) / 1e9, 1)
+        for kind in ("attn", "step", "flushed"):
+            row["valu_over_mfma_%s" % kind] = round(row["valu_%s_us" % kind] / row["mfma_%s_us" % kind], 4)
+        print(json.dumps(row), flush=True)
+        rows.append(row)
+        del q, k, v, out, ws
+        torch.cuda.empty_cache()
+    os.makedirs(outdir, exist_ok=True)
+    keys = list(rows[0].keys())
+    with open(os.path.join(outdir, "attn_score_ab.csv"), "w") as f:
+        f.write(",".join(keys) + "\n")
+        for r in rows:
+            f.write(",".join(str(r[x]) for x in keys) + "\n")
+    with open(os.path.join(outdir, "attn_score_ab.json"), "w") as f:
+        json.dump(rows, f, indent=1)
+
+
 def next_profile(outdir: str, iters: int = 20, warmup: int = 3):
     """A short, profiler-friendly run of the other kernels: vd_gemm_bf16 on
     the four Llama-3-8B-shaped projections at M = 1, 16, 64, 256, 257 and
@@ -737,6 +827,14 @@ def main():
                     help="instead of the bench line, time a decode layer step (qkv GEMM, KV append, "
                          "attention, o_proj / gate_up / down GEMMs) over (batch, tokens per request) "
                          "and write DIR/decode_layer_surface.csv")
+    ap.add_argument("--score-ab", metavar="DIR", default=None,
+                    help="instead of the bench line, time the matrix-core and vector-ALU score "
+                         "paths against each other, interleaved, and write DIR/attn_score_ab.csv")
+    ap.add_argument("--ab-workloads", default="tiny_b4,llama8b_b64,chat_b256,gqa8_b128,long_b16",
+                    help="comma-separated workloads for --score-ab")
+    ap.add_argument("--score", choices=("mfma", "valu"), default="mfma",
+                    help="score path of the bench line's attention kernel (valu: "
+                         "VD_FLAG_SCORE_VALU, for profiling that path)")
     ap.add_argument("--surface", metavar="DIR", default=None,
                     help="instead of the bench line, measure the latency surface over "
                          "(batch, tokens per request) and write DIR/decode_latency_surface.{csv,md}")
@@ -757,6 +855,9 @@ def main():
 
     if args.surface:
         latency_surface(args.surface)
+        return
+    if args.score_ab:
+        score_ab(args.score_ab, [x for x in args.ab_workloads.split(",") if x])
         return
     if args.layer_surface:
         layer_surface(args.layer_surface)
@@ -799,6 +900,7 @@ def main():
     B, Hq, Hkv, maxp = c["num_seqs"], c["n_q_heads"], c["n_kv_heads"], c["max_pages_per_seq"]
     ws = vd.alloc_workspace(B, Hq, Hkv, maxp)
     stream = torch.cuda.current_stream()
+    SF = vd.VD_FLAG_SCORE_VALU if args.score == "valu" else 0
     torch.cuda.synchronize()
 
     def step(ev0=None, ev1=None):
@@ -806,11 +908,11 @@ def main():
         # events, the same two stages called one by one around the attention
         # launch
         if ev0 is None:
-            vd.vd_decode_attn(q, k, v, pt, sl, out, c["scale"], ws, stream=stream)
+            vd.vd_decode_attn(q, k, v, pt, sl, out, c["scale"], ws, flags=SF, stream=stream)
             return
         ev0.record(stream)
-        vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws, flags=vd.VD_FLAG_SELF_PLAN,
-                             stream=stream)
+        vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws,
+                             flags=vd.VD_FLAG_SELF_PLAN | SF, stream=stream)
         ev1.record(stream)
         vd.vd_decode_combine(out, Hkv, maxp, ws, stream=stream)
 
@@ -840,8 +942,8 @@ def main():
     # around each launch would also count its dispatch and end-of-kernel
     # write-back, a few microseconds each.
     def attn_only():
-        vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws, flags=vd.VD_FLAG_SELF_PLAN,
-                             stream=stream)
+        vd.vd_decode_partial(q, k, v, pt, sl, out, c["scale"], ws,
+                             flags=vd.VD_FLAG_SELF_PLAN | SF, stream=stream)
 
     for _ in range(args.warmup):
         attn_only()
@@ -930,7 +1032,7 @@ def main():
     algo_bytes = (kvb + q.numel() * 2 + out.numel() * 2 + int(P.sum()) * 4 + B * 4)
     achieved = algo_bytes / (attn_avg_ms * 1e-3) / 1e9
     value = kvb / (ms_step * 1e-3) / 1e9
-    traffic = committed_traffic(w.name)
+    traffic = committed_traffic(w.name) if args.score == "mfma" else None
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -975,7 +1077,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "description": w.description, "num_seqs": B,
                    "n_q_heads": Hq, "n_kv_heads": Hkv, "head_dim": 128, "page_size": 16,
-                   "n_kv_tokens": c["n_kv"], "kv_bytes": kvb, "seed": 0},
+                   "n_kv_tokens": c["n_kv"], "kv_bytes": kvb, "seed": 0, "score": args.score},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                      "traffic": traffic, "kernel": "attn_kernel",

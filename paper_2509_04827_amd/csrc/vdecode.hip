@@ -102,6 +102,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 // The workspace header is the step record of the C ABI (vd_step_info):
@@ -452,7 +453,8 @@ struct AttnArgs {
 enum { MODE_BF16 = 0, MODE_F32 = 1, MODE_GATHER = 2 };
 
 struct Tile {
-    u32x4 k[4];   // K[token r][d 8(4kk+grp) .. +8]          (score MFMA A operand)
+    u32x4 k[4];   // MFMA score: K[token r][d 8(4kk+grp) .. +8]  (A operand)
+                  // vector-ALU score: K[token 4grp+j][d 8r .. 8r+8], as v
     u32x4 v[4];   // V[token 4grp+j][d 8r .. 8r+8], j = 0..3  (raw rows)
 };
 
@@ -464,6 +466,9 @@ __device__ inline u32x4 ldg16_stream(const uint16_t *p)
 
 __device__ inline u32x4 ldg16(const uint16_t *p) { return *(const u32x4 *)p; }
 
+// VS: the vector-ALU score layout of K (the rows of V's layout; koff must
+// then equal voff).
+template <bool VS = false>
 __device__ inline void load_tile(Tile &T, const uint16_t *kpage, const uint16_t *vpage,
                                  unsigned koff, unsigned voff, unsigned row)
 {
@@ -474,7 +479,7 @@ __device__ inline void load_tile(Tile &T, const uint16_t *kpage, const uint16_t 
         vp[j] = vpage + voff + j * row;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk)
-        T.k[kk] = ldg16_stream(kp + 32 * kk);
+        T.k[kk] = ldg16_stream(VS ? kp + kk * row : kp + 32 * kk);
 #pragma unroll
     for (int j = 0; j < 4; ++j)
         T.v[j] = ldg16_stream(vp[j]);
@@ -785,6 +790,95 @@ __device__ inline void load_q(const AttnArgs &a, int b, int g, int lane, u32x4 (
         qreg[kk] = ldg16(qrow + 32 * kk);
 }
 
+// Registers of a wave's Q operand: four 16-byte slices for the MFMA score,
+// one per head for the vector-ALU score.
+template <int G, bool VS>
+constexpr int kQRegs = VS ? G : 4;
+
+// Q for the vector-ALU score: slot s holds head s ^ (r & (G-1)) at d
+// 8r .. 8r+8, every head in an order rotated by the lane's own head bits.
+template <int G>
+__device__ inline void load_q_valu(const AttnArgs &a, int b, int g, int lane, u32x4 (&qv)[G])
+{
+    const int r = lane & 15;
+    const uint16_t *qrow = a.q + ((size_t)b * a.Hq + g * G) * kHeadDim + 8 * r;
+#pragma unroll
+    for (int s = 0; s < G; ++s)
+        qv[s] = ldg16(qrow + (size_t)(s ^ (r & (G - 1))) * kHeadDim);
+}
+
+template <bool VS, int G>
+__device__ inline void load_q_any(const AttnArgs &a, int b, int g, int lane,
+                                  u32x4 (&qreg)[kQRegs<G, VS>])
+{
+    if constexpr (VS)
+        load_q_valu<G>(a, b, g, lane, qreg);
+    else
+        load_q<G>(a, b, g, lane, qreg);
+}
+
+template <int CTRL>
+__device__ inline float dpp_row(float x)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x),
+                                                                 CTRL, 0xF, 0xF, false));
+}
+
+// One exchange of the row reduction over LIVE slots: with more than one, the
+// lane keeps the even slots, each plus its partner lane's next odd slot
+// (which holds the same head, the partner's rotation differing in this
+// step's bit); with one, a plain sum.
+template <int CTRL, int LIVE, int G>
+__device__ inline void row_fold(float (&v)[4][G])
+{
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if constexpr (LIVE > 1) {
+#pragma unroll
+            for (int t = 0; t < LIVE / 2; ++t)
+                v[j][t] = v[j][2 * t] + dpp_row<CTRL>(v[j][2 * t + 1]);
+        } else {
+            v[j][0] += dpp_row<CTRL>(v[j][0]);
+        }
+    }
+}
+
+// Q.K^T of a page's 16 tokens against G <= 8 heads on the vector ALU, the
+// alternative to the MFMA score: lane (r, grp) forms the dot products of
+// tokens 4grp+j over its eight dimensions 8r .. 8r+8 with each head (bf16
+// pairs, fp32 sums), and the 16 lanes of row grp add up their slices through
+// DPP row exchanges (quad permutes for lane bits 0 and 1, row rotations by 4
+// and 8 lanes): the first log2 G exchanges halve the live head slots, the rest
+// sum.  Lane r ends with head r & (G-1), so s[j] is token 4grp+j of head r,
+// the layout of the MFMA score.
+template <int G>
+__device__ inline f32x4 score_valu(const Tile &T, const u32x4 (&qv)[G])
+{
+    static_assert(G <= 8, "head bits must stay within three lane bits");
+    float v[4][G];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int s = 0; s < G; ++s) {
+            float acc = 0.f;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                // element copies first: a bit cast of a vector element
+                // itself reads element 0 in this compiler
+                const unsigned kw = T.k[j][e], qw = qv[s][e];
+                acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, kw),
+                                                      __builtin_bit_cast(bf16x2, qw), acc, false);
+            }
+            v[j][s] = acc;
+        }
+    }
+    row_fold<0xB1, G, G>(v);                          // quad_perm [1,0,3,2]: lane ^ 1
+    row_fold<0x4E, (G > 1 ? G / 2 : 1), G>(v);        // quad_perm [2,3,0,1]: lane ^ 2
+    row_fold<0x124, (G > 2 ? G / 4 : 1), G>(v);       // row_ror:4
+    row_fold<0x128, (G > 4 ? G / 8 : 1), G>(v);       // row_ror:8: lane ^ 8
+    return f32x4{v[0][0], v[1][0], v[2][0], v[3][0]};
+}
+
 // Copy-through gather of one piece (je - jb <= kMaxRangeTiles) for KV head
 // g = q * HW + hi; its page ids were loaded during the previous piece.
 __device__ inline void gather_piece(const AttnArgs &a, const Piece &pc, const PageIds &ids, int hi,
@@ -845,9 +939,9 @@ __device__ inline void gather_piece(const AttnArgs &a, const Piece &pc, const Pa
 // an exact count.  fetch_next() walks to the next piece and loads its page
 // ids and Q operand (into nids / the caller's registers) before the first
 // step.
-template <int G, int PH, typename Fetch>
+template <int G, bool VS, int PH, typename Fetch>
 __device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageIds &ids,
-                                 const u32x4 (&qreg)[4], Tile (&ring)[2], Fetch &&fetch_next,
+                                 const u32x4 (&qreg)[kQRegs<G, VS>], Tile (&ring)[2], Fetch &&fetch_next,
                                  const PageIds &nids, const Piece &nxt, int hi, int lane,
                                  float *entry, float2 *entry_ml)
 {
@@ -857,8 +951,8 @@ __device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageI
     const int g = pc.q * a.HW + hi, jb = pc.jb, je = pc.je, L = pc.L;
     const unsigned row = (unsigned)Hkv * kHeadDim;        // elements per token row
     const size_t page_elems = (size_t)kPage * row;
-    const unsigned koff = r * row + g * kHeadDim + 8 * grp;
     const unsigned voff = 4 * grp * row + g * kHeadDim + 8 * r;
+    const unsigned koff = VS ? voff : r * row + g * kHeadDim + 8 * grp;
     const uint16_t *kb = a.k, *vb = a.v;
     const int np = je - jb;
 
@@ -873,11 +967,15 @@ __device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageI
 
     auto page_step = [&](const Tile &T, int j) {
         f32x4 s = {0.f, 0.f, 0.f, 0.f};
+        if constexpr (VS) {
+            s = score_valu<G>(T, qreg);
+        } else {
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-            s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, T.k[kk]), __builtin_bit_cast(bf16x8, qreg[kk]),
-                s, 0, 0, 0);
+            for (int kk = 0; kk < 4; ++kk)
+                s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(bf16x8, T.k[kk]), __builtin_bit_cast(bf16x8, qreg[kk]),
+                    s, 0, 0, 0);
+        }
         // s[i]: token 4grp+i, head r
         float sc[4];
 #pragma unroll
@@ -927,13 +1025,15 @@ __device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageI
 
     auto load_in = [&](Tile &T, int jn) {   // page jn of this piece
         const int pg = ids.get(jn - jb);
-        load_tile(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems, koff, voff, row);
+        load_tile<VS>(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems, koff, voff,
+                      row);
     };
     auto load_next = [&](Tile &T) {         // first page of the next piece
         const int ng = nxt.q * a.HW + hi;
         const int pg = nids.get(0);
-        load_tile(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems,
-                  r * row + ng * kHeadDim + 8 * grp, 4 * grp * row + ng * kHeadDim + 8 * r, row);
+        const unsigned nv = 4 * grp * row + ng * kHeadDim + 8 * r;
+        load_tile<VS>(T, kb + (size_t)pg * page_elems, vb + (size_t)pg * page_elems,
+                      VS ? nv : r * row + ng * kHeadDim + 8 * grp, nv, row);
     };
     constexpr int A = PH, B = PH ^ 1;
     if (np >= 2) {
@@ -996,7 +1096,7 @@ __device__ inline int attn_piece(const AttnArgs &a, const Piece &pc, const PageI
 // length), page ids and Q operand are fetched at the start of a piece, and
 // its first page while the piece's last page is consumed, so the K/V stream
 // of a wave runs on across piece boundaries.
-template <int G, int MODE, bool SELF>
+template <int G, int MODE, bool SELF, bool VS>
 __device__ inline void attn_body(const AttnArgs &a)
 {
     const int lane = threadIdx.x & 63;
@@ -1089,22 +1189,24 @@ __device__ inline void attn_body(const AttnArgs &a)
             }
             n_res = 0;
         };
-        u32x4 qreg[4];
-        load_q<G>(a, cur.b, cur.q * HW + hi, lane, qreg);
+        constexpr int NQ = kQRegs<G, VS>;
+        u32x4 qreg[NQ];
+        load_q_any<VS, G>(a, cur.b, cur.q * HW + hi, lane, qreg);
         Tile ring[2];
         {   // first page of the first piece
             const unsigned row = (unsigned)a.Hkv * kHeadDim;
             const int r = lane & 15, grp = lane >> 4, g = cur.q * HW + hi;
             const size_t pg = (size_t)ids.get(0) * kPage * row;
-            load_tile(ring[0], a.k + pg, a.v + pg, r * row + g * kHeadDim + 8 * grp,
-                      4 * grp * row + g * kHeadDim + 8 * r, row);
+            const unsigned voff = 4 * grp * row + g * kHeadDim + 8 * r;
+            load_tile<VS>(ring[0], a.k + pg, a.v + pg,
+                          VS ? voff : r * row + g * kHeadDim + 8 * grp, voff, row);
         }
         int ph = 0;
         while (true) {
             Piece nxt;
             bool more = false;
             PageIds nids;
-            u32x4 nq[4];
+            u32x4 nq[NQ];
             auto fetch_next = [&]() {
                 more = walk.next(a, Hg, nxt);
                 if (!more) {   // last piece: the final prefetch re-reads its last page
@@ -1112,15 +1214,15 @@ __device__ inline void attn_body(const AttnArgs &a)
                     nxt.jb = cur.je - 1;
                 }
                 nids = load_page_ids(a.pt + (size_t)nxt.b * a.pt_stride, nxt.jb, nxt.je, lane);
-                load_q<G>(a, nxt.b, nxt.q * HW + hi, lane, nq);
+                load_q_any<VS, G>(a, nxt.b, nxt.q * HW + hi, lane, nq);
             };
             if (n_res == kDefer)
                 flush();
             float *entry = s_res[hi][n_res];
             float2 *entry_ml = s_ml[hi][n_res];
             const int flip =
-                ph == 0 ? attn_piece<G, 0>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml)
-                        : attn_piece<G, 1>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml);
+                ph == 0 ? attn_piece<G, VS, 0>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml)
+                        : attn_piece<G, VS, 1>(a, cur, ids, qreg, ring, fetch_next, nids, nxt, hi, lane, entry, entry_ml);
             {
                 const int g = cur.q * HW + hi;
                 const bool whole = cur.jb == 0 && cur.je == (cur.L + kPage - 1) / kPage;
@@ -1134,10 +1236,9 @@ __device__ inline void attn_body(const AttnArgs &a)
             ph ^= flip;
             cur = nxt;
             ids = nids;
-            qreg[0] = nq[0];
-            qreg[1] = nq[1];
-            qreg[2] = nq[2];
-            qreg[3] = nq[3];
+#pragma unroll
+            for (int i = 0; i < NQ; ++i)
+                qreg[i] = nq[i];
         }
         flush();
     }
@@ -1145,7 +1246,7 @@ __device__ inline void attn_body(const AttnArgs &a)
 
 // The first workgroup stamps the step record with the real-time and
 // shader-clock counters at its start and end.
-template <int G, int MODE, bool SELF>
+template <int G, int MODE, bool SELF, bool VS = false>
 __global__ void __launch_bounds__(kAttnMaxThreads)
 attn_kernel(const AttnArgs a)
 {
@@ -1154,7 +1255,7 @@ attn_kernel(const AttnArgs a)
         a.hdr->t_start = __builtin_amdgcn_s_memrealtime();
         a.hdr->clk_start = __builtin_amdgcn_s_memtime();
     }
-    attn_body<G, MODE, SELF>(a);
+    attn_body<G, MODE, SELF, VS>(a);
     if (stamp) {
         a.hdr->t_end = __builtin_amdgcn_s_memrealtime();
         a.hdr->clk_end = __builtin_amdgcn_s_memtime();
@@ -1392,10 +1493,12 @@ int check_shapes(int num_seqs, int n_q_heads, int n_kv_heads, int head_dim, int 
         return VD_ERROR_INVALID_VALUE;
     if (n_q_heads % n_kv_heads != 0)
         return VD_ERROR_INVALID_VALUE;
-    if (flags & ~(VD_FLAG_OUT_F32 | VD_FLAG_SELF_PLAN | VD_FLAG_RANGE_MASK))
+    if (flags & ~(VD_FLAG_OUT_F32 | VD_FLAG_SELF_PLAN | VD_FLAG_SCORE_VALU | VD_FLAG_RANGE_MASK))
         return VD_ERROR_INVALID_VALUE;
     if (head_dim != kHeadDim || page_size != kPage || !supported_g(n_q_heads / n_kv_heads) ||
         num_seqs > kMaxSeqs)
+        return VD_ERROR_NOT_SUPPORTED;
+    if ((flags & VD_FLAG_SCORE_VALU) && n_q_heads / n_kv_heads > 8)
         return VD_ERROR_NOT_SUPPORTED;
     // 32-bit in-page offsets, tile counts, token counts, output rows and
     // partial slots (fewer than (maxp + 1) * B * Hkv)
@@ -1438,11 +1541,27 @@ int num_cus(int *out)
 }
 
 // The attention kernel for G, output mode and planning: planned (tables
-// from the planner kernel) or self-planned (whole step).
-const void *attn_kernel_ptr(int G, int mode, bool self)
+// from the planner kernel) or self-planned (whole step); `valu` selects the
+// vector-ALU score, self-planned and G <= 8 only.
+const void *attn_kernel_ptr(int G, int mode, bool self, bool valu = false)
 {
     if (mode == MODE_GATHER)
-        return self ? nullptr : (const void *)attn_kernel<1, MODE_GATHER, false>;
+        return self || valu ? nullptr : (const void *)attn_kernel<1, MODE_GATHER, false>;
+    if (valu) {
+        if (!self)
+            return nullptr;
+#define VD_KV(g)                                                                               \
+    (mode == MODE_F32 ? (const void *)attn_kernel<g, MODE_F32, true, true>                      \
+                      : (const void *)attn_kernel<g, MODE_BF16, true, true>)
+        switch (G) {
+        case 1: return VD_KV(1);
+        case 2: return VD_KV(2);
+        case 4: return VD_KV(4);
+        case 8: return VD_KV(8);
+        default: return nullptr;
+        }
+#undef VD_KV
+    }
 #define VD_K(g)                                                                                \
     (self ? (mode == MODE_F32 ? (const void *)attn_kernel<g, MODE_F32, true>                  \
                               : (const void *)attn_kernel<g, MODE_BF16, true>)                \
@@ -1548,13 +1667,14 @@ int enqueue_plan(const int32_t *seq_lens, int num_seqs, int G, int n_kv_heads,
     return launch_status();
 }
 
-int enqueue_attn(const AttnArgs &args, int G, int mode, bool self, hipStream_t stream)
+int enqueue_attn(const AttnArgs &args, int G, int mode, bool self, hipStream_t stream,
+                 bool valu = false)
 {
     int groups = 0;
     int st = resident_attn_groups(G, mode, args.HW, &groups);
     if (st)
         return st;
-    const void *k = attn_kernel_ptr(G, mode, self);
+    const void *k = attn_kernel_ptr(G, mode, self, valu);
     if (!k)
         return VD_ERROR_NOT_SUPPORTED;
     AttnArgs copy = args;
@@ -1685,7 +1805,7 @@ int enqueue_partial(const void *q, const void *k_pages, const void *v_pages,
     a.seq_lens = seq_lens;
     a.out = out;
     a.zero_empty = zero_empty ? 1 : 0;
-    return enqueue_attn(a, G, out_mode(flags), self, stream);
+    return enqueue_attn(a, G, out_mode(flags), self, stream, (flags & VD_FLAG_SCORE_VALU) != 0);
 }
 
 // The whole step: the self-planned attention kernel, then the combine kernel

@@ -89,6 +89,8 @@ def test_argument_errors(entry):
     assert call_attn(fn, S=32, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     assert call_attn(fn, Hq=24, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     assert call_attn(fn, Hq=256, Hkv=8, **ok) == vd.VD_ERROR_NOT_SUPPORTED   # G = 32
+    # the vector-ALU score keeps a row's heads within three lane bits: G <= 8
+    assert call_attn(fn, Hq=128, Hkv=8, flags=vd.VD_FLAG_SCORE_VALU, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     assert call_attn(fn, B=9000, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     # output rows (request, query head) and partial slots must fit 32 bits
     assert call_attn(fn, B=8192, Hq=262144, Hkv=16384, maxp=1, **ok) == vd.VD_ERROR_NOT_SUPPORTED
