@@ -626,8 +626,8 @@ def layer_surface(outdir: str, reps: int = 5):
 
 def score_ab(outdir: str, workloads, rounds: int = 7, iters: int = 50, flushed: int = 30):
     """The two score paths of the attention kernel against each other: the
-    matrix-core score (default) and the vector-ALU one (VD_FLAG_SCORE_VALU:
-    bf16 pair dot products summed across lanes by DPP).  Per workload (seed
+    vector-ALU score (the default for G <= 8: bf16 pair dot products summed
+    across lanes by DPP) and the matrix-core one (VD_FLAG_SCORE_MFMA).  Per workload (seed
     0, the bench's inputs), in one process on the same inputs and clocks:
     `rounds` rounds that alternate which path goes first, each timing
     `iters` back-to-back attention launches (the self-planned kernel alone,
@@ -644,8 +644,7 @@ def score_ab(outdir: str, workloads, rounds: int = 7, iters: int = 50, flushed: 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
-    V = vd.VD_FLAG_SCORE_VALU
-    paths = (("mfma", 0), ("valu", V))
+    paths = (("mfma", vd.VD_FLAG_SCORE_MFMA), ("valu", 0))
     fbuf = torch.zeros(1 << 30, dtype=torch.uint8, device=dev)
     fsink = torch.zeros(4, dtype=torch.int32, device=dev)
     rows = []
@@ -832,9 +831,9 @@ def main():
                          "paths against each other, interleaved, and write DIR/attn_score_ab.csv")
     ap.add_argument("--ab-workloads", default="tiny_b4,llama8b_b64,chat_b256,gqa8_b128,long_b16",
                     help="comma-separated workloads for --score-ab")
-    ap.add_argument("--score", choices=("mfma", "valu"), default="mfma",
-                    help="score path of the bench line's attention kernel (valu: "
-                         "VD_FLAG_SCORE_VALU, for profiling that path)")
+    ap.add_argument("--score", choices=("default", "mfma"), default="default",
+                    help="score path of the bench line's attention kernel (mfma: "
+                         "VD_FLAG_SCORE_MFMA, for profiling that path)")
     ap.add_argument("--surface", metavar="DIR", default=None,
                     help="instead of the bench line, measure the latency surface over "
                          "(batch, tokens per request) and write DIR/decode_latency_surface.{csv,md}")
@@ -900,7 +899,7 @@ def main():
     B, Hq, Hkv, maxp = c["num_seqs"], c["n_q_heads"], c["n_kv_heads"], c["max_pages_per_seq"]
     ws = vd.alloc_workspace(B, Hq, Hkv, maxp)
     stream = torch.cuda.current_stream()
-    SF = vd.VD_FLAG_SCORE_VALU if args.score == "valu" else 0
+    SF = vd.VD_FLAG_SCORE_MFMA if args.score == "mfma" else 0
     torch.cuda.synchronize()
 
     def step(ev0=None, ev1=None):
@@ -1032,7 +1031,7 @@ def main():
     algo_bytes = (kvb + q.numel() * 2 + out.numel() * 2 + int(P.sum()) * 4 + B * 4)
     achieved = algo_bytes / (attn_avg_ms * 1e-3) / 1e9
     value = kvb / (ms_step * 1e-3) / 1e9
-    traffic = committed_traffic(w.name) if args.score == "mfma" else None
+    traffic = committed_traffic(w.name) if args.score == "default" else None
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -1077,7 +1076,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "description": w.description, "num_seqs": B,
                    "n_q_heads": Hq, "n_kv_heads": Hkv, "head_dim": 128, "page_size": 16,
-                   "n_kv_tokens": c["n_kv"], "kv_bytes": kvb, "seed": 0, "score": args.score},
+                   "n_kv_tokens": c["n_kv"], "kv_bytes": kvb, "seed": 0,
+                   "score": "mfma" if args.score == "mfma" or Hq // Hkv > 8 else "valu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                      "traffic": traffic, "kernel": "attn_kernel",

@@ -77,14 +77,14 @@ typedef enum vd_status {
  * needs no vd_decode_plan before it; ignored by the other calls
  * (vd_decode_attn always plans this way). */
 #define VD_FLAG_SELF_PLAN (1u << 1)
-/* Compute the scores Q.K^T on the vector ALU (bf16 pair dot products, then
- * DPP sums across the lanes that hold one token's dimensions) instead of the
- * matrix cores; the rest of the step is unchanged.  For measuring the two
- * score paths against each other.  Self-planned launches only
- * (vd_decode_attn, vd_decode_attn_noalloc, vd_decode_partial with
- * VD_FLAG_SELF_PLAN) and G = n_q_heads / n_kv_heads <= 8, else
- * VD_ERROR_NOT_SUPPORTED. */
-#define VD_FLAG_SCORE_VALU (1u << 2)
+/* Score path.  For G = n_q_heads / n_kv_heads <= 8 the scores Q.K^T are
+ * computed on the vector ALU (bf16 pair dot products, then DPP sums across
+ * the lanes that hold one token's dimensions); for G = 16, and for any G with
+ * this flag, on the matrix cores (an MFMA tile of 16 tokens by the G heads).
+ * The rest of the step is the same.  The workspace, the plan and the
+ * ranges do not depend on the path.  For measuring the two paths against
+ * each other. */
+#define VD_FLAG_SCORE_MFMA (1u << 2)
 /* bits 8..15: cut the step's (page, KV head) tiles into ranges of this many
  * tiles (1..255) instead of the automatic partition (0).  Changes where the
  * split-K boundaries fall, not the result beyond rounding; for tests.  The

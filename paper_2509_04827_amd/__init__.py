@@ -38,7 +38,7 @@ VD_ERROR_SCRATCH_LIMIT = 5
 VD_NOALLOC_SCRATCH_BYTES = 64 << 20
 VD_FLAG_OUT_F32 = 1 << 0
 VD_FLAG_SELF_PLAN = 1 << 1
-VD_FLAG_SCORE_VALU = 1 << 2   # vector-ALU score (measurement of the score paths)
+VD_FLAG_SCORE_MFMA = 1 << 2   # matrix-core score for G <= 8 (measurement of the score paths)
 VD_FLAG_RANGE_SHIFT = 8
 
 EXPORTS = ("vd_status_string", "vd_decode_workspace_size", "vd_decode_attn", "vd_decode_attn_noalloc", "vd_decode_plan",

@@ -40,16 +40,24 @@
 //                   workgroup first scans the request lengths in LDS to find
 //                   its ranges' start and boundary records (the planner's
 //                   arithmetic, so both cut identical ranges).  Per page:
-//                     K rows are loaded straight into MFMA A operands (lane =
-//                     token row); scores = K Q^T with v_mfma_f32_16x16x32_bf16
-//                     against the group's G query heads (columns past G
-//                     repeat head G-1 and are never stored);
+//                     scores = K Q^T against the group's G query heads,
+//                     for G <= 8 on the vector ALU: K rows are loaded like V
+//                     (lane r, row block grp: tokens 4grp+j, dimensions
+//                     8r..8r+8), each lane forms bf16 pair dot products
+//                     with every head, and DPP row exchanges sum a token's
+//                     16 slices while scattering the heads so that lane r
+//                     ends with head r (score_valu); for G = 16, or on
+//                     request, on the matrix cores: K rows go straight into
+//                     the A operands of v_mfma_f32_16x16x32_bf16 (lane =
+//                     token row; columns past G repeat head G-1 and are
+//                     never stored).  Both leave the scores in the same
+//                     layout (lane r, row block grp: tokens 4grp+i of head r);
 //                     online softmax in fp32 (exp2 domain, lazy rescaling);
 //                     V rows are loaded coalesced (4 rows x 256 B per
 //                     instruction) and transposed in registers with byte
 //                     permutes into the A operand of
 //                     v_mfma_f32_16x16x16_bf16, whose B operand is P exactly
-//                     as the score MFMA left it (P split into bf16 hi + lo).
+//                     as the score left it (P split into bf16 hi + lo).
 //                   A wave's K/V stream runs on across pieces: the next
 //                   piece's bounds come from scalar loads of request
 //                   lengths, its page ids
@@ -62,8 +70,9 @@
 //                   a range boundary cuts (zeros for requests without
 //                   tokens).
 //
-// All arithmetic is fp32; bf16 is only the storage type of Q/K/V, the MFMA
-// operand type, and the optional output type.
+// All arithmetic is fp32; bf16 is only the storage type of Q/K/V, the
+// operand type of the MFMAs and pair dot products, and the optional output
+// type.
 
 #include <hip/hip_runtime.h>
 
@@ -843,8 +852,8 @@ __device__ inline void row_fold(float (&v)[4][G])
     }
 }
 
-// Q.K^T of a page's 16 tokens against G <= 8 heads on the vector ALU, the
-// alternative to the MFMA score: lane (r, grp) forms the dot products of
+// Q.K^T of a page's 16 tokens against G <= 8 heads on the vector ALU (the
+// default score path for those G): lane (r, grp) forms the dot products of
 // tokens 4grp+j over its eight dimensions 8r .. 8r+8 with each head (bf16
 // pairs, fp32 sums), and the 16 lanes of row grp add up their slices through
 // DPP row exchanges (quad permutes for lane bits 0 and 1, row rotations by 4
@@ -1484,6 +1493,10 @@ bool supported_g(int G) { return G == 1 || G == 2 || G == 4 || G == 8 || G == 16
 
 int forced_tiles(unsigned flags) { return (int)((flags & VD_FLAG_RANGE_MASK) >> VD_FLAG_RANGE_SHIFT); }
 
+// Score path: the vector ALU for G <= 8 unless VD_FLAG_SCORE_MFMA, else the
+// matrix cores.
+bool valu_score(int G, unsigned flags) { return G <= 8 && !(flags & VD_FLAG_SCORE_MFMA); }
+
 // Shape checks shared by every entry point.
 int check_shapes(int num_seqs, int n_q_heads, int n_kv_heads, int head_dim, int page_size,
                  int max_pages_per_seq, unsigned flags)
@@ -1493,12 +1506,10 @@ int check_shapes(int num_seqs, int n_q_heads, int n_kv_heads, int head_dim, int 
         return VD_ERROR_INVALID_VALUE;
     if (n_q_heads % n_kv_heads != 0)
         return VD_ERROR_INVALID_VALUE;
-    if (flags & ~(VD_FLAG_OUT_F32 | VD_FLAG_SELF_PLAN | VD_FLAG_SCORE_VALU | VD_FLAG_RANGE_MASK))
+    if (flags & ~(VD_FLAG_OUT_F32 | VD_FLAG_SELF_PLAN | VD_FLAG_SCORE_MFMA | VD_FLAG_RANGE_MASK))
         return VD_ERROR_INVALID_VALUE;
     if (head_dim != kHeadDim || page_size != kPage || !supported_g(n_q_heads / n_kv_heads) ||
         num_seqs > kMaxSeqs)
-        return VD_ERROR_NOT_SUPPORTED;
-    if ((flags & VD_FLAG_SCORE_VALU) && n_q_heads / n_kv_heads > 8)
         return VD_ERROR_NOT_SUPPORTED;
     // 32-bit in-page offsets, tile counts, token counts, output rows and
     // partial slots (fewer than (maxp + 1) * B * Hkv)
@@ -1540,19 +1551,19 @@ int num_cus(int *out)
     return VD_SUCCESS;
 }
 
-// The attention kernel for G, output mode and planning: planned (tables
-// from the planner kernel) or self-planned (whole step); `valu` selects the
-// vector-ALU score, self-planned and G <= 8 only.
-const void *attn_kernel_ptr(int G, int mode, bool self, bool valu = false)
+// The attention kernel for G, output mode, planning (planned: tables from
+// the planner kernel; self-planned: the whole step) and score path (`valu`:
+// the vector-ALU score, G <= 8).
+const void *attn_kernel_ptr(int G, int mode, bool self, bool valu)
 {
     if (mode == MODE_GATHER)
         return self || valu ? nullptr : (const void *)attn_kernel<1, MODE_GATHER, false>;
     if (valu) {
-        if (!self)
-            return nullptr;
 #define VD_KV(g)                                                                               \
-    (mode == MODE_F32 ? (const void *)attn_kernel<g, MODE_F32, true, true>                      \
-                      : (const void *)attn_kernel<g, MODE_BF16, true, true>)
+    (self ? (mode == MODE_F32 ? (const void *)attn_kernel<g, MODE_F32, true, true>              \
+                              : (const void *)attn_kernel<g, MODE_BF16, true, true>)            \
+          : (mode == MODE_F32 ? (const void *)attn_kernel<g, MODE_F32, false, true>             \
+                              : (const void *)attn_kernel<g, MODE_BF16, false, true>))
         switch (G) {
         case 1: return VD_KV(1);
         case 2: return VD_KV(2);
@@ -1630,10 +1641,14 @@ int resident_attn_groups(int G, int mode, int HW, int *groups)
     int st = num_cus(&cus);
     if (st)
         return st;
-    // planned and self-planned kernels must agree on R (it sets the ranges)
+    // planned and self-planned kernels of both score paths must agree on R
+    // (it sets the ranges)
     int per_cu = kAttnWavesPerCU;
-    for (int self = 0; self < (mode == MODE_GATHER ? 1 : 2); ++self) {
-        const void *k = attn_kernel_ptr(G, mode, self != 0);
+    for (int v = 0; v < 4; ++v) {
+        const bool self = v & 1, valu = v & 2;
+        if ((mode == MODE_GATHER && (self || valu)) || (valu && !valu_score(G, 0)))
+            continue;
+        const void *k = attn_kernel_ptr(G, mode, self, valu);
         if (!k)
             return VD_ERROR_NOT_SUPPORTED;
         int n = 0;
@@ -1667,8 +1682,7 @@ int enqueue_plan(const int32_t *seq_lens, int num_seqs, int G, int n_kv_heads,
     return launch_status();
 }
 
-int enqueue_attn(const AttnArgs &args, int G, int mode, bool self, hipStream_t stream,
-                 bool valu = false)
+int enqueue_attn(const AttnArgs &args, int G, int mode, bool self, bool valu, hipStream_t stream)
 {
     int groups = 0;
     int st = resident_attn_groups(G, mode, args.HW, &groups);
@@ -1805,7 +1819,7 @@ int enqueue_partial(const void *q, const void *k_pages, const void *v_pages,
     a.seq_lens = seq_lens;
     a.out = out;
     a.zero_empty = zero_empty ? 1 : 0;
-    return enqueue_attn(a, G, out_mode(flags), self, stream, (flags & VD_FLAG_SCORE_VALU) != 0);
+    return enqueue_attn(a, G, out_mode(flags), self, valu_score(G, flags), stream);
 }
 
 // The whole step: the self-planned attention kernel, then the combine kernel
@@ -2035,7 +2049,7 @@ int vd_decode_gather(const void *k_pages, const void *v_pages, const int32_t *pa
     a.seq_lens = seq_lens;
     a.out = k_out;
     a.out2 = v_out;
-    return enqueue_attn(a, 1, MODE_GATHER, false, stream);
+    return enqueue_attn(a, 1, MODE_GATHER, false, false, stream);
 }
 
 int vd_kv_append(const void *k_new, const void *v_new, void *k_pages, void *v_pages,

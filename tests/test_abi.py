@@ -49,6 +49,9 @@ def test_workspace_size_rules():
     # planning in the attention kernel needs no other workspace
     assert ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_SELF_PLAN) == ws(4, 32, 8, 128, 16, 63)
     assert ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_SELF_PLAN | vd.VD_FLAG_OUT_F32) == ws(4, 32, 8, 128, 16, 63)
+    # the score path does not change the workspace, for any G
+    for hq in (8, 32, 64, 128):
+        assert ws(4, hq, 8, 128, 16, 63, vd.VD_FLAG_SCORE_MFMA) == ws(4, hq, 8, 128, 16, 63) > 0
     # one tile per range: up to one partial per (page, KV head) plus one per segment
     small = ws(4, 32, 8, 128, 16, 63, vd.VD_FLAG_RANGE_TILES(1))
     assert small >= (4 * 63 * 8 + 4 * 8) * 4 * 128 * 4
@@ -89,8 +92,6 @@ def test_argument_errors(entry):
     assert call_attn(fn, S=32, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     assert call_attn(fn, Hq=24, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     assert call_attn(fn, Hq=256, Hkv=8, **ok) == vd.VD_ERROR_NOT_SUPPORTED   # G = 32
-    # the vector-ALU score keeps a row's heads within three lane bits: G <= 8
-    assert call_attn(fn, Hq=128, Hkv=8, flags=vd.VD_FLAG_SCORE_VALU, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     assert call_attn(fn, B=9000, **ok) == vd.VD_ERROR_NOT_SUPPORTED
     # output rows (request, query head) and partial slots must fit 32 bits
     assert call_attn(fn, B=8192, Hq=262144, Hkv=16384, maxp=1, **ok) == vd.VD_ERROR_NOT_SUPPORTED

@@ -1,15 +1,16 @@
-"""The vector-ALU score path (VD_FLAG_SCORE_VALU) against the fp64 oracle,
-through the C ABI.
+"""The two score paths of the attention kernel, through the C ABI.
 
-With the flag the scores Q.K^T come from bf16 pair dot products summed in
-fp32 across the 16 lanes that hold a token's dimensions (DPP row exchanges)
-instead of the matrix cores; loads, softmax, P.V and the combine are the
-MFMA path's.  So the same gates hold (fp32 out within the precision canary,
-bf16 out within an ulp), the closed forms stay exact (one token, one-hot
-scores), the output does not depend on page placement or on what fills the
-pages past a request's end, and the whole step equals the staged
-self-planned calls bit for bit.  G = 16 and the planned attention launch
-are refused.
+For G <= 8 the default path computes the scores Q.K^T on the vector ALU:
+bf16 pair dot products summed in fp32 across the 16 lanes that hold a
+token's dimensions (DPP row exchanges).  VD_FLAG_SCORE_MFMA computes them on
+the matrix cores instead (the only path for G = 16).  Loads, softmax, P.V and
+the combine are shared.  The default path is what every other parity test
+runs; here the matrix-core path is held to the same bar against the fp64
+oracle (gates and precision canary, bf16 within an ulp), the closed forms stay
+exact (one token, one-hot scores), the output does not depend on page
+placement or on what fills the pages past a request's end, and the whole step
+equals the staged calls (planner kernel or self-planned) bit for bit.  The two
+paths agree with each other to fp32 rounding.
 """
 import numpy as np
 import pytest
@@ -23,17 +24,17 @@ from workloads import ORDER, make_case
 pytestmark = pytest.mark.gpu
 
 DEV = P.DEV
-V = vd.VD_FLAG_SCORE_VALU
+M = vd.VD_FLAG_SCORE_MFMA
 
 
 @pytest.mark.parametrize("name", ORDER)
-def test_workload_parity_valu(name):
-    P.say("case: workload %s seed 0, vector-ALU score" % name)
+def test_workload_parity_mfma(name):
+    P.say("case: workload %s seed 0, matrix-core score" % name)
     c = make_case(name, seed=0, fill="nan")
     d = P.dev_case(c)
     ref = P.ref_of(c)
-    P.check_f32(P.run_gpu(d, torch.float32, flags=V), ref, name + " valu", canary=True)
-    P.check_bf16(P.run_gpu(d, torch.bfloat16, flags=V), ref, name + " valu")
+    P.check_f32(P.run_gpu(d, torch.float32, flags=M), ref, name + " mfma", canary=True)
+    P.check_bf16(P.run_gpu(d, torch.bfloat16, flags=M), ref, name + " mfma")
 
 
 def test_valu_and_mfma_scores_agree():
@@ -41,45 +42,51 @@ def test_valu_and_mfma_scores_agree():
     orders: their outputs agree to fp32 rounding."""
     c = make_case("chat_b256", seed=1, fill="nan")
     d = P.dev_case(c)
-    a = P.run_gpu(d, torch.float32).cpu().double()
-    b = P.run_gpu(d, torch.float32, flags=V).cpu().double()
+    a = P.run_gpu(d, torch.float32, flags=M).cpu().double()
+    b = P.run_gpu(d, torch.float32).cpu().double()
     rel = ((a - b).norm() / a.norm()).item()
     P.say("case: chat_b256 seed 1, valu vs mfma rel-L2 %.3e max-abs %.3e"
           % (rel, (a - b).abs().max().item()))
     assert rel <= 1e-6 and (a - b).abs().max().item() <= 1e-5
 
 
-@pytest.mark.parametrize("G,hkv", [(1, 4), (2, 4), (4, 2), (8, 2), (8, 8), (4, 16), (1, 16)])
-def test_gqa_ratios_valu(G, hkv):
-    """Every G the DPP reduction serves (1, 2, 4, 8: one to three head bits
-    scattered over the lanes, the rest summed), with empty, one-token and
-    page-boundary lengths and a long request."""
-    P.say("case: valu G=%d Hkv=%d" % (G, hkv))
+@pytest.mark.parametrize("G,hkv", [(1, 4), (2, 4), (4, 2), (8, 2), (8, 8), (4, 16), (1, 16), (16, 2)])
+@pytest.mark.parametrize("path", ["default", "mfma"])
+def test_gqa_ratios_both_paths(G, hkv, path):
+    """Every G on both paths (the DPP reduction scatters one to three head
+    bits over the lanes and sums the rest; G = 16 is the matrix cores' on
+    both), with empty, one-token and page-boundary lengths and a long
+    request."""
+    flags = M if path == "mfma" else 0
+    P.say("case: %s score G=%d Hkv=%d" % (path, G, hkv))
     c = P.custom([1, 20, 0, 300, 2222, 64, 15, 16, 17, 4097], hq=G * hkv, hkv=hkv, seed=113 + G)
     d = P.dev_case(c)
     ref = P.ref_of(c)
-    got = P.run_gpu(d, flags=V)
+    got = P.run_gpu(d, flags=flags)
     assert torch.equal(got[2], torch.zeros_like(got[2]))
-    P.check_f32(got, ref, "valu G=%d" % G, canary=True)
-    P.check_bf16(P.run_gpu(d, torch.bfloat16, flags=V), ref, "valu G=%d" % G)
+    P.check_f32(got, ref, "%s G=%d" % (path, G), canary=True)
+    P.check_bf16(P.run_gpu(d, torch.bfloat16, flags=flags), ref, "%s G=%d" % (path, G))
+    if G == 16:   # one path for G = 16: the flag changes nothing
+        other = P.run_gpu(d, flags=flags ^ M)
+        assert torch.equal(got.view(torch.int32).cpu(), other.view(torch.int32).cpu())
 
 
-def test_single_token_is_v_row_valu():
-    P.say("case: valu L=1 x 37 requests")
+def test_single_token_is_v_row_mfma():
+    P.say("case: mfma score, L=1 x 37 requests")
     c = P.custom([1] * 37, hq=32, hkv=8, seed=3)
     d = P.dev_case(c)
     pt = c["page_table"].numpy()
     expect = np.repeat(P.bits(c["v_pages"])[pt[:, 0], 0], 4, axis=1)
-    assert np.array_equal(P.bits(P.run_gpu(d, torch.bfloat16, flags=V).cpu()), expect)
+    assert np.array_equal(P.bits(P.run_gpu(d, torch.bfloat16, flags=M).cpu()), expect)
 
 
 @pytest.mark.parametrize("split", [0, 3])
-def test_one_hot_is_v_row_valu(split):
-    """Scores that single out one token per (request, head) exactly: the
-    vector-ALU sum must reach the same -inf-free maximum as the MFMA one."""
+def test_one_hot_is_v_row_mfma(split):
+    """Scores that single out one token per (request, head): the output is
+    that token's V row exactly on the matrix-core path too."""
     lengths = [1, 40, 300, 17, 2000, 5000, 16, 33]
     hot = [0, 39, 150, 16, 1999, 2500, 0, 32]
-    P.say("case: valu one-hot split=%d" % split)
+    P.say("case: mfma score one-hot split=%d" % split)
     c = pins.onehot_case(lengths, 32, 8, 11, hot)
     q = torch.from_numpy(c["q"].view(np.int16)).view(torch.bfloat16)
     k = torch.from_numpy(c["k"].view(np.int16)).view(torch.bfloat16)
@@ -88,7 +95,7 @@ def test_one_hot_is_v_row_valu(split):
              page_table=torch.from_numpy(c["pt"]).to(DEV), seq_lens=torch.from_numpy(c["L"]).to(DEV),
              scale=c["scale"], num_seqs=len(lengths), n_q_heads=32, n_kv_heads=8,
              max_pages_per_seq=c["pt"].shape[1])
-    flags = V | (vd.VD_FLAG_RANGE_TILES(split) if split else 0)
+    flags = M | (vd.VD_FLAG_RANGE_TILES(split) if split else 0)
     got = P.run_gpu(d, torch.float32, flags=flags).cpu().numpy()
     for b, t in enumerate(hot):
         vrow = c["v"][c["pt"][b, t // 16], t % 16]
@@ -96,9 +103,9 @@ def test_one_hot_is_v_row_valu(split):
         assert np.array_equal(got[b], expect), b
 
 
-def test_fill_and_placement_invariance_valu():
+def test_fill_and_placement_invariance_mfma():
     """NaN or zero past each request's end, pages permuted: the same bits."""
-    P.say("case: valu NaN vs zero fill, page permutation, determinism")
+    P.say("case: mfma score, NaN vs zero fill, page permutation, determinism")
     lengths = [5, 17, 31, 250, 1111, 4097, 1]
     a = P.custom(lengths, seed=7, fill="nan", shuffle=False)
     z = P.custom(lengths, seed=7, fill="zero", shuffle=False)
@@ -109,22 +116,23 @@ def test_fill_and_placement_invariance_valu():
     b["k_pages"][perm] = a["k_pages"]
     b["v_pages"][perm] = a["v_pages"]
     b["page_table"] = perm.to(torch.int32)[a["page_table"].long()]
-    x1 = P.run_gpu(P.dev_case(a), flags=V).cpu()
-    x2 = P.run_gpu(P.dev_case(a), flags=V).cpu()
-    y = P.run_gpu(P.dev_case(z), flags=V).cpu()
-    w = P.run_gpu(P.dev_case(b), flags=V).cpu()
+    x1 = P.run_gpu(P.dev_case(a), flags=M).cpu()
+    x2 = P.run_gpu(P.dev_case(a), flags=M).cpu()
+    y = P.run_gpu(P.dev_case(z), flags=M).cpu()
+    w = P.run_gpu(P.dev_case(b), flags=M).cpu()
     assert torch.isfinite(x1).all()
     for other in (x2, y, w):
         assert torch.equal(x1.view(torch.int32), other.view(torch.int32))
-    P.check_f32(x1, P.ref_of(a), "valu fill/placement", canary=True)
+    P.check_f32(x1, P.ref_of(a), "mfma fill/placement", canary=True)
 
 
 @pytest.mark.parametrize("case", ["short_mixed", "split_many", "mixed_forced7", "many_pieces"])
-def test_whole_equals_staged_valu(case):
-    """vd_decode_attn against vd_decode_partial (self-planned) plus
-    vd_decode_combine, both with the vector-ALU score: bit for bit; and
-    against the oracle."""
-    flags = V
+def test_whole_equals_staged_mfma(case):
+    """With the matrix-core score: vd_decode_attn against the planner kernel
+    plus the planned vd_decode_partial plus vd_decode_combine, and against
+    the self-planned vd_decode_partial plus vd_decode_combine: bit for bit;
+    and against the oracle."""
+    flags = M
     hq, hkv = 32, 8
     if case == "short_mixed":
         lengths = [0, 5, 0, 64, 0, 17, 1, 33]
@@ -137,7 +145,7 @@ def test_whole_equals_staged_valu(case):
         rng = np.random.default_rng(58)
         lengths = [int(x) for x in rng.choice([1, 3, 16, 17, 40, 100], 3000)]
         hq, hkv = 16, 2
-    P.say("case: valu whole vs staged %s (%d requests)" % (case, len(lengths)))
+    P.say("case: mfma score, whole vs staged %s (%d requests)" % (case, len(lengths)))
     c = P.custom(lengths, hq=hq, hkv=hkv, seed=122)
     d = P.dev_case(c)
     B, maxp = c["num_seqs"], c["max_pages_per_seq"]
@@ -145,35 +153,17 @@ def test_whole_equals_staged_valu(case):
         whole = P.run_gpu(d, dt, flags=flags)
         ws = vd.alloc_workspace(B, hq, hkv, maxp, flags)
         staged = torch.full(d["q"].shape, float("nan"), dtype=dt, device=DEV)
+        vd.vd_decode_plan(d["seq_lens"], hq, hkv, maxp, ws, flags=flags)
         vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
-                             staged, d["scale"], ws, flags=flags | vd.VD_FLAG_SELF_PLAN)
+                             staged, d["scale"], ws, flags=flags)
         vd.vd_decode_combine(staged, hkv, maxp, ws, flags=flags)
+        selfp = torch.full(d["q"].shape, float("nan"), dtype=dt, device=DEV)
+        vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
+                             selfp, d["scale"], ws, flags=flags | vd.VD_FLAG_SELF_PLAN)
+        vd.vd_decode_combine(selfp, hkv, maxp, ws, flags=flags)
         torch.cuda.synchronize()
         iv = torch.int32 if dt == torch.float32 else torch.int16
         assert torch.equal(whole.view(iv).cpu(), staged.view(iv).cpu()), case
+        assert torch.equal(whole.view(iv).cpu(), selfp.view(iv).cpu()), case
         if dt == torch.float32:
-            P.check_f32(whole, P.ref_of(c), "valu " + case, canary=True)
-
-
-def test_valu_refusals_on_device():
-    """G = 16, and the planned attention launch (no VD_FLAG_SELF_PLAN):
-    refused before anything is launched."""
-    c = P.custom([33, 100], hq=16, hkv=1, seed=5)
-    d = P.dev_case(c)
-    out = torch.full(d["q"].shape, float("nan"), dtype=torch.float32, device=DEV)
-    ws = vd.alloc_workspace(2, 16, 1, c["max_pages_per_seq"])
-    with pytest.raises(vd.VdError) as e:
-        vd.vd_decode_attn(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"], out,
-                          d["scale"], ws, flags=V)
-    assert e.value.status == vd.VD_ERROR_NOT_SUPPORTED
-    c = P.custom([33, 100], hq=32, hkv=8, seed=5)
-    d = P.dev_case(c)
-    out = torch.full(d["q"].shape, float("nan"), dtype=torch.float32, device=DEV)
-    ws = vd.alloc_workspace(2, 32, 8, c["max_pages_per_seq"], V)
-    vd.vd_decode_plan(d["seq_lens"], 32, 8, c["max_pages_per_seq"], ws, flags=V)
-    with pytest.raises(vd.VdError) as e:
-        vd.vd_decode_partial(d["q"], d["k_pages"], d["v_pages"], d["page_table"], d["seq_lens"],
-                             out, d["scale"], ws, flags=V)
-    assert e.value.status == vd.VD_ERROR_NOT_SUPPORTED
-    torch.cuda.synchronize()
-    assert torch.isnan(out).all()
+            P.check_f32(whole, P.ref_of(c), "mfma " + case, canary=True)
