@@ -24,12 +24,13 @@ HIPCC_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall",
 ]
-# per source: the attention kernels keep MFMA accumulators in ordinary VGPRs
-# (the online-softmax rescale touches them with VALU ops, which would
-# otherwise copy AGPRs back and forth); the GEMM's large tiles need the AGPRs
+# per source: MFMA accumulators in ordinary VGPRs.  The attention kernels'
+# online-softmax rescale touches them with VALU ops, and the GEMM tiles'
+# accumulators fit the VGPRs; in AGPRs the compiler copies them back and forth
+# inside the K loop (over 200 accumulator moves per stage of the LDS-fed tiles)
 SRC_FLAGS = {
     "vdecode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
-    "gemm.hip": [],
+    "gemm.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

@@ -13,7 +13,10 @@
 //     x and w tiles of each K stage (BK columns) are loaded with 16-byte loads
 //     (whole 128- or 256-byte row pieces) into registers, and from there into
 //     one of two LDS buffers (rows padded by 16 bytes against bank
-//     conflicts), P stages ahead of the one being multiplied;
+//     conflicts), P stages ahead of the one being multiplied; the two
+//     largest tiles (128 x 128 and 256 x 128 for larger batches) load their
+//     stages straight from memory into a ring of LDS slots instead
+//     (gemm_dma_kernel), so the pipeline depth costs no registers;
 //   * each wave multiplies its (BN/WN) x (BM/WM) part of the tile with
 //     v_mfma_f32_16x16x32_bf16, the w fragment as the A operand (lane = output
 //     column) and the x fragment as B (lane = batch row), so the accumulator
@@ -235,6 +238,184 @@ gemm_tile_kernel(const GemmArgs a)
     }
 }
 
+// s_waitcnt with vmcnt(N) and lgkmcnt(0): this wave's loads older than its
+// last N are done, and its LDS reads have returned.
+template <int N>
+__device__ inline void wait_vm_lds()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
+}
+
+// Larger-batch tile with its stages loaded straight into LDS.  A stage is BK
+// columns (BK = 32 or 64: 64- or 128-byte rows of CH = BK / 8 chunks of 16
+// bytes) of the tile's BM x rows and BN w rows.  Each
+// global_load_lds_dwordx4 writes one 1 KiB block of LDS, lane l's 16 bytes
+// at the instruction's LDS base + 16 l, i.e. 64 / CH consecutive rows; lane
+// l loads row l / CH of the block and the chunk that puts row rho's chunk c
+// at slot c ^ swz(rho) (swz = rho mod 8 for 8 chunks, (rho / 2) mod 4 for
+// 4), so that the MFMA fragment reads (16 consecutive rows, one chunk) fall
+// in distinct banks.  NSLOT stages form a ring in LDS, up to NSLOT - 1 in
+// flight while one is multiplied.  No registers carry the stages, so the
+// pipeline depth costs LDS only.  The waits are explicit: before stage k is
+// read, the wave waits for its own loads of stage k (the later stages' loads
+// stay in flight) and for its LDS reads; a barrier without a memory fence
+// then makes stage k complete for every wave, and only after it is the slot
+// of stage k - 1 refilled.  Loads past the slice's end re-read its last
+// stage into a slot that is never read again, so every iteration issues the
+// same loads and the wait counts are constants.
+template <int CH>
+__device__ inline int chunk_swz(int row)
+{
+    return CH == 8 ? (row & 7) : ((row >> 1) & 3);
+}
+
+template <int BM, int BN, int BK, int WM, int WN, int NSLOT, int MODE>
+__global__ void __launch_bounds__(kThreads)
+gemm_dma_kernel(const GemmArgs a)
+{
+    constexpr int CH = BK / 8;                   // 16-byte chunks per row
+    constexpr int RPI = 64 / CH;                 // rows per load instruction
+    constexpr int ROWS = BM + BN;                // x rows, then w rows, per stage
+    constexpr int SLOT = ROWS * BK;              // bf16 elements per stage
+    constexpr int IPW = ROWS / RPI / 4;          // load instructions per wave and stage
+    constexpr int H = BK / 32;                   // MFMA k-steps per stage
+    constexpr int TM = BM / WM, TN = BN / WN;
+    constexpr int FM = TM / 16, FN = TN / 16;
+    static_assert(BK == 32 || BK == 64, "stage width");
+    static_assert(WM * WN == kThreads / 64, "four waves");
+    static_assert(ROWS % (4 * RPI) == 0 && BM % RPI == 0 && TM % 16 == 0 && TN % 16 == 0, "shape");
+    static_assert((NSLOT - 1) * IPW < 64, "vmcnt");
+    __shared__ __attribute__((aligned(1024))) uint16_t lds[NSLOT * SLOT];
+
+    const int i = blockIdx.x, TMc = a.tiles_m, G = a.groups;
+    const int full = G / 8 * 8;
+    int tm, g;
+    if (i < full * TMc) {
+        const int sg = i / (8 * TMc), rem = i - sg * 8 * TMc;
+        tm = rem >> 3;
+        g = sg * 8 + (rem & 7);
+    } else {
+        const int j = i - full * TMc, r8 = G - full;
+        tm = j / r8;
+        g = full + (j - tm * r8);
+    }
+    const int tn = g / a.S, s = g - tn * a.S;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int M = a.M, N = a.N, K = a.K;
+    const int nk = a.kslice / BK;
+
+    const int t = threadIdx.x, lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+    // this lane's source for each of its load instructions at stage 0; rows
+    // past M repeat row M - 1 (loaded, never stored).  A block starts at a
+    // multiple of RPI rows, so swz of the lane's row is swz(lane / CH).
+    const int chunk = (lane % CH) ^ chunk_swz<CH>(lane / CH);
+    const uint16_t *src[IPW];
+#pragma unroll
+    for (int j = 0; j < IPW; ++j) {
+        const int rho = (wave * IPW + j) * RPI + lane / CH;
+        const uint16_t *row = rho < BM ? a.x + (size_t)min(m0 + rho, M - 1) * K
+                                       : a.w + (size_t)(n0 + rho - BM) * K;
+        src[j] = row + (size_t)s * a.kslice + chunk * 8;
+    }
+    auto issue = [&](int kt) {
+        const size_t off = (size_t)min(kt, nk - 1) * BK;
+        uint16_t *dst = lds + (kt % NSLOT) * SLOT + wave * IPW * RPI * BK;
+#pragma unroll
+        for (int j = 0; j < IPW; ++j)
+            __builtin_amdgcn_global_load_lds((const void *)(src[j] + off),
+                                             (__attribute__((address_space(3))) void *)(dst + j * RPI * BK),
+                                             16, 0, 0);
+    };
+
+    f32x4 acc[FN][FM];
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+            acc[fn][fm] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int wn = wave % WN, wm = wave / WN;
+    const int r = lane & 15, kq = lane >> 4;
+    struct Frags {
+        u32x4 a[FN], b[FM];
+    };
+    // the fragments of k-step h (32 columns: stage h / H, its half h % H)
+    auto read = [&](Frags &f, int h) {
+        const uint16_t *base = lds + ((h / H) % NSLOT) * SLOT;
+        const int sl = ((4 * (h % H) + kq) ^ chunk_swz<CH>(r)) * 8;   // this lane's chunk slot
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+            f.a[fn] = *(const u32x4 *)(base + (BM + wn * TN + 16 * fn + r) * BK + sl);
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+            f.b[fm] = *(const u32x4 *)(base + (wm * TM + 16 * fm + r) * BK + sl);
+    };
+    auto mma = [&](const Frags &f) {
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+            for (int fm = 0; fm < FM; ++fm)
+                acc[fn][fm] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                    __builtin_bit_cast(bf16x8, f.a[fn]), __builtin_bit_cast(bf16x8, f.b[fm]),
+                    acc[fn][fm], 0, 0, 0);
+    };
+    // k-step h: the next step's fragments are read (after the wait and
+    // barrier for the next stage, when it starts one) while this step's
+    // MFMAs run.  After that barrier every wave has read all of stage
+    // h / H, and its slot is refilled with stage h / H + NSLOT.
+    auto step = [&](int h, const Frags &cur, Frags &nxt) {
+        if ((h + 1) % H == 0) {
+            asm volatile("" ::: "memory");
+            wait_vm_lds<(NSLOT - 2) * IPW>();   // this wave's next stage is in LDS, cur is read
+            __builtin_amdgcn_s_barrier();       // ... every wave's
+            asm volatile("" ::: "memory");
+            issue(h / H + NSLOT);               // into this stage's slot
+        }
+        read(nxt, h + 1);
+        mma(cur);
+    };
+
+#pragma unroll
+    for (int p = 0; p < NSLOT; ++p)   // every slot
+        issue(p);
+    asm volatile("" ::: "memory");
+    wait_vm_lds<(NSLOT - 1) * IPW>();   // stage 0
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    Frags f0, f1;
+    read(f0, 0);
+    for (int h = 0; h < nk * H; h += 2) {   // nk * H is even: K slices are whole 512 columns
+        step(h, f0, f1);
+        step(h + 1, f1, f0);
+    }
+    wait_vm_lds<0>();   // the re-reads past the end land before the wave ends
+
+    // acc[fn][fm][e]: column n0 + wn*TN + 16 fn + 4 kq + e of row
+    // m0 + wm*TM + 16 fm + r
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+        const int m = m0 + wm * TM + 16 * fm + r;
+        if (m >= M)
+            continue;
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+            const int n = n0 + wn * TN + 16 * fn + 4 * kq;
+            const f32x4 v = acc[fn][fm];
+            if constexpr (MODE == OUT_PART) {
+                *(f32x4 *)(a.part + ((size_t)s * M + m) * N + n) = v;
+            } else if constexpr (MODE == OUT_F32) {
+                *(f32x4 *)((float *)a.y + (size_t)m * N + n) = v;
+            } else {
+                *(u32x2 *)((uint16_t *)a.y + (size_t)m * N + n) =
+                    u32x2{(unsigned)bf16_rne(v[0]) | ((unsigned)bf16_rne(v[1]) << 16),
+                          (unsigned)bf16_rne(v[2]) | ((unsigned)bf16_rne(v[3]) << 16)};
+            }
+        }
+    }
+}
+
 // y[e] = sum over slices s = 0 .. S-1 (in order) of part[s][e], four per
 // thread; the S loads are all issued before the first add.
 template <int MODE, int S>
@@ -264,19 +445,21 @@ gemm_reduce_kernel(const float *__restrict__ part, void *__restrict__ y, size_t 
 // ---------------------------------------------------------------- host side
 // The tile configurations (index = VD_GEMM_FLAG_TILE's argument), with the
 // two figures the automatic choice weighs them by, measured on MI355X: how
-// fast the tile streams weights relative to 5.7 TB/s once its workgroups fill
-// the device, and its matrix-core throughput (PFLOP/s) on a full device.
+// fast the tile streams weights relative to 5.574 TB/s once its workgroups
+// fill the device, and its matrix-core throughput (PFLOP/s) on a full device.
 struct TileCfg {
     int bm, bn, bk;
     double stream_eff, pflops;
 };
 constexpr TileCfg kTiles[] = {
-    {16, 64, 128, 1.15, 1.0},    // 0: four waves over the columns
-    {32, 64, 128, 0.90, 0.65},   // 1
-    {48, 64, 128, 0.90, 1.0},    // 2
-    {64, 64, 128, 0.95, 0.33},   // 3
-    {64, 128, 64, 1.05, 0.50},   // 4: 2 x 2 waves
-    {128, 128, 64, 1.20, 0.80},  // 5
+    {16, 64, 128, 0.787, 1.0},     // 0: four waves over the columns
+    {32, 64, 128, 1.2, 0.649},     // 1
+    {48, 64, 128, 0.696, 1.0},     // 2
+    {64, 64, 128, 0.674, 0.459},   // 3
+    {64, 128, 64, 0.91, 0.47},     // 4: 2 x 2 waves
+    {128, 128, 64, 0.853, 0.44},   // 5
+    {128, 128, 64, 0.906, 0.766},  // 6: stages loaded straight into LDS, four in a ring
+    {256, 128, 64, 0.908, 0.902},  // 7: the same, 2 x 2 waves of 128 x 64, three stages
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
@@ -295,12 +478,14 @@ void launch_tile(int cfg, const GemmArgs &g, dim3 grid, hipStream_t stream)
         else
             hipLaunchKernelGGL((gemm_tile_kernel<64, 128, 64, 2, 2, 2, MODE, false>), grid, block, 0, stream, g);
         break;
-    default:
+    case 5:
         if (g.tiles_m == 1)
             hipLaunchKernelGGL((gemm_tile_kernel<128, 128, 64, 2, 2, 2, MODE>), grid, block, 0, stream, g);
         else
             hipLaunchKernelGGL((gemm_tile_kernel<128, 128, 64, 2, 2, 2, MODE, false>), grid, block, 0, stream, g);
         break;
+    case 6: hipLaunchKernelGGL((gemm_dma_kernel<128, 128, 64, 2, 2, 4, MODE>), grid, block, 0, stream, g); break;
+    default: hipLaunchKernelGGL((gemm_dma_kernel<256, 128, 64, 2, 2, 3, MODE>), grid, block, 0, stream, g); break;
     }
 }
 
@@ -344,23 +529,24 @@ long long plan_groups(const TileCfg &c, int M, int N, int S)
 }
 
 // Estimated time (microseconds) of a plan on MI355X: a fixed 4 us, plus the
-// larger of the weight stream (5.7 TB/s times the tile's streaming
+// larger of the weight stream (5.574 TB/s times the tile's streaming
 // efficiency, scaled down while its workgroups fill less than 192 CUs) and
 // the matrix-core time (the tile's throughput, scaled by the CUs it fills,
 // on the rows padded to whole tiles); K slices add the fp32 partials' round
-// trip at 1.6 TB/s and the reduction kernel (5 us); every 512 workgroups past
-// the first 512 add 19 us.  The constants were fitted to a sweep of the four
-// Llama-3-8B-shaped projections over M = 1 .. 1024 with weights that do not
-// fit the caches (the choice costs 1.6% over the best plan on average).
+// trip at 3.0 TB/s and the reduction kernel (2.888 us); every 512 workgroups
+// past the first 512 add 3.314 us.  The constants were fitted to a sweep of
+// every tile and 1, 2, 4 or 8 slices at the four Llama-3-8B-shaped
+// projections and 30 batch sizes M = 1 .. 1024, with weights that do not fit
+// the caches: the chosen plan costs 2.8% more than the best one on average.
 double plan_cost(const TileCfg &c, int M, int N, int K, int S)
 {
     const double groups = (double)plan_groups(c, M, N, S);
     const double mpad = (double)((M + c.bm - 1) / c.bm) * c.bm;
-    const double t_w = (double)N * K * 2.0 / (5.7e6 * c.stream_eff * std::min(1.0, groups / 192.0));
+    const double t_w = (double)N * K * 2.0 / (5.574e6 * c.stream_eff * std::min(1.0, groups / 192.0));
     const double t_mfma = 2.0 * mpad * N * K / (c.pflops * 1e9 * std::min(1.0, groups / kTargetCUs));
-    const double t_part = S > 1 ? (double)S * M * N * 8.0 / 1.6e6 + 5.0 : 0.0;
+    const double t_part = S > 1 ? (double)S * M * N * 8.0 / 3.0e6 + 2.888 : 0.0;
     const double waves = std::ceil(groups / 512.0);
-    return 4.0 + std::max(t_w, t_mfma) + t_part + 19.0 * (waves - 1.0);
+    return 4.0 + std::max(t_w, t_mfma) + t_part + 3.314 * (waves - 1.0);
 }
 
 // The automatic choice, from the sizes alone: the cheapest plan by

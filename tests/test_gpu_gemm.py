@@ -32,7 +32,7 @@ SHAPES = [(1, 4096, 4096), (7, 6144, 4096), (9, 4096, 4096), (16, 512, 512),
 
 # Every tile configuration with 1, 2, 8 and 16 K slices at two row counts
 # (37: several narrow row tiles; 300: a partial last tile of every size).
-FORCED = [(M, c, l) for M in (37, 300) for c in range(6) for l in (0, 1, 3, 4)]
+FORCED = [(M, c, l) for M in (37, 300) for c in range(8) for l in (0, 1, 3, 4)]
 
 
 def inputs(M, N, K, seed):
