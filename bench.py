@@ -41,20 +41,19 @@ WORKLOAD = "chat_b256"
 
 
 def kernel_source_hash() -> str:
-    """Hash of the attention library's code (sources and build flags), with
-    comments and whitespace removed, so that counters taken on one build
-    are reported only for the same code."""
+    """Hash of what the attention kernels are built from: their source and the
+    header, with comments and whitespace removed, and the compiler flags of
+    that source, so that counters taken on one build are reported only for
+    the same code."""
+    from paper_2509_04827_amd import build as vbuild
     h = hashlib.sha256()
-    for rel in ("paper_2509_04827_amd/csrc/vdecode.hip", "include/vdecode.h",
-                "paper_2509_04827_amd/build.py"):
+    for rel in ("paper_2509_04827_amd/csrc/vdecode.hip", "include/vdecode.h"):
         with open(os.path.join(ROOT, rel)) as f:
             text = f.read()
-        if rel.endswith(".py"):
-            text = re.sub(r"#[^\n]*", "", text)
-        else:
-            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-            text = re.sub(r"//[^\n]*", "", text)
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
         h.update("".join(text.split()).encode())
+    h.update(" ".join(vbuild.HIPCC_FLAGS + vbuild.SRC_FLAGS["vdecode.hip"]).encode())
     return h.hexdigest()[:16]
 
 

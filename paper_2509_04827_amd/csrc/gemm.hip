@@ -445,21 +445,21 @@ gemm_reduce_kernel(const float *__restrict__ part, void *__restrict__ y, size_t 
 // ---------------------------------------------------------------- host side
 // The tile configurations (index = VD_GEMM_FLAG_TILE's argument), with the
 // two figures the automatic choice weighs them by, measured on MI355X: how
-// fast the tile streams weights relative to 5.574 TB/s once its workgroups
+// fast the tile streams weights relative to 5.482 TB/s once its workgroups
 // fill the device, and its matrix-core throughput (PFLOP/s) on a full device.
 struct TileCfg {
     int bm, bn, bk;
     double stream_eff, pflops;
 };
 constexpr TileCfg kTiles[] = {
-    {16, 64, 128, 0.787, 1.0},     // 0: four waves over the columns
+    {16, 64, 128, 1.167, 1.0},     // 0: four waves over the columns
     {32, 64, 128, 1.2, 0.649},     // 1
-    {48, 64, 128, 0.696, 1.0},     // 2
-    {64, 64, 128, 0.674, 0.459},   // 3
-    {64, 128, 64, 0.91, 0.47},     // 4: 2 x 2 waves
-    {128, 128, 64, 0.853, 0.44},   // 5
-    {128, 128, 64, 0.906, 0.766},  // 6: stages loaded straight into LDS, four in a ring
-    {256, 128, 64, 0.908, 0.902},  // 7: the same, 2 x 2 waves of 128 x 64, three stages
+    {48, 64, 128, 0.746, 1.0},     // 2
+    {64, 64, 128, 0.714, 0.46},    // 3
+    {64, 128, 64, 0.991, 0.456},   // 4: 2 x 2 waves
+    {128, 128, 64, 0.853, 0.429},  // 5
+    {128, 128, 64, 1.2, 0.73},     // 6: stages loaded straight into LDS, four in a ring
+    {256, 128, 64, 0.908, 1.0},    // 7: the same, 2 x 2 waves of 128 x 64, three stages
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
@@ -529,24 +529,24 @@ long long plan_groups(const TileCfg &c, int M, int N, int S)
 }
 
 // Estimated time (microseconds) of a plan on MI355X: a fixed 4 us, plus the
-// larger of the weight stream (5.574 TB/s times the tile's streaming
+// larger of the weight stream (5.482 TB/s times the tile's streaming
 // efficiency, scaled down while its workgroups fill less than 192 CUs) and
 // the matrix-core time (the tile's throughput, scaled by the CUs it fills,
 // on the rows padded to whole tiles); K slices add the fp32 partials' round
-// trip at 3.0 TB/s and the reduction kernel (2.888 us); every 512 workgroups
-// past the first 512 add 3.314 us.  The constants were fitted to a sweep of
+// trip at 2.648 TB/s and the reduction kernel (2.686 us); every 512
+// workgroups past the first 512 add 19.3 us.  The constants were fitted to a sweep of
 // every tile and 1, 2, 4 or 8 slices at the four Llama-3-8B-shaped
 // projections and 30 batch sizes M = 1 .. 1024, with weights that do not fit
-// the caches: the chosen plan costs 2.8% more than the best one on average.
+// the caches: the chosen plan costs 2.7% more than the best one on average.
 double plan_cost(const TileCfg &c, int M, int N, int K, int S)
 {
     const double groups = (double)plan_groups(c, M, N, S);
     const double mpad = (double)((M + c.bm - 1) / c.bm) * c.bm;
-    const double t_w = (double)N * K * 2.0 / (5.574e6 * c.stream_eff * std::min(1.0, groups / 192.0));
+    const double t_w = (double)N * K * 2.0 / (5.482e6 * c.stream_eff * std::min(1.0, groups / 192.0));
     const double t_mfma = 2.0 * mpad * N * K / (c.pflops * 1e9 * std::min(1.0, groups / kTargetCUs));
-    const double t_part = S > 1 ? (double)S * M * N * 8.0 / 3.0e6 + 2.888 : 0.0;
+    const double t_part = S > 1 ? (double)S * M * N * 8.0 / 2.648e6 + 2.686 : 0.0;
     const double waves = std::ceil(groups / 512.0);
-    return 4.0 + std::max(t_w, t_mfma) + t_part + 3.314 * (waves - 1.0);
+    return 4.0 + std::max(t_w, t_mfma) + t_part + 19.328 * (waves - 1.0);
 }
 
 // The automatic choice, from the sizes alone: the cheapest plan by
