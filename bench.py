@@ -712,7 +712,7 @@ def score_ab(outdir: str, workloads, rounds: int = 7, iters: int = 50, flushed: 
         json.dump(rows, f, indent=1)
 
 
-def next_profile(outdir: str, iters: int = 20, warmup: int = 3):
+def next_profile(outdir: str, iters: int = 20, warmup: int = 3, only=None, hipblaslt: bool = False):
     """A short, profiler-friendly run of the other kernels: vd_gemm_bf16 on
     the four Llama-3-8B-shaped projections at M = 1, 16, 64, 256, 257 and
     1024 (cold weights: a ring of copies over 1 GiB), then
@@ -721,7 +721,11 @@ def next_profile(outdir: str, iters: int = 20, warmup: int = 3):
     before it, so a kernel trace splits into one burst per case in the order
     of next_profile.csv, and starts with one vd_stream_read of 4 KiB (a
     marker dispatch, so counter runs without timestamps split by case too).
-    Optionally ends with --copy-calibration copies."""
+    Optionally ends with --copy-calibration copies.
+
+    `only` = (shape, M) runs that one GEMM case and no KV append; with
+    `hipblaslt` the case calls torch.matmul instead of vd_gemm_bf16 (the
+    same operands), to set the two kernels' counters side by side."""
     import numpy as np
     import torch
 
@@ -752,35 +756,42 @@ def next_profile(outdir: str, iters: int = 20, warmup: int = 3):
         return e0.elapsed_time(e1) * 1e3 / iters
 
     for name, N, K in GEMM_SHAPES:
+        if only is not None and name != only[0]:
+            continue
         # a ring of weight copies over 1 GiB: every call reads weights that
         # no cache holds, as a decode step does
         ring_n = max(2, -(-(1 << 30) // (N * K * 2)))
         ring = [torch.randn((N, K), generator=gen, device=dev).to(torch.bfloat16) for _ in range(ring_n)]
-        for M in NEXT_PROFILE_M:
+        for M in (NEXT_PROFILE_M if only is None else (only[1],)):
             x = torch.randn((M, K), generator=gen, device=dev).to(torch.bfloat16)
             y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
             ws = torch.empty(max(16, vd.vd_gemm_workspace_size(M, N, K)), dtype=torch.uint8, device=dev)
             cnt = [0]
 
             def call():
-                vd.vd_gemm_bf16(x, ring[cnt[0] % ring_n], y, ws, stream=stream)
+                if hipblaslt:
+                    torch.matmul(x, ring[cnt[0] % ring_n].t(), out=y)
+                else:
+                    vd.vd_gemm_bf16(x, ring[cnt[0] % ring_n], y, ws, stream=stream)
                 cnt[0] += 1
             us = burst(call)
-            rows.append(dict(case="gemm_%s_M%d" % (name, M), calls=iters, us_events=round(us, 2),
+            rows.append(dict(case="gemm_%s_M%d%s" % (name, M, "_hipblaslt" if hipblaslt else ""),
+                             calls=iters, us_events=round(us, 2),
                              algorithmic_bytes=(N * K + M * K + M * N) * 2))
         del ring
         torch.cuda.empty_cache()
-    B, Hkv, S, maxp = 256, 8, 16, 4
-    pages = torch.randperm(B * maxp, generator=torch.Generator().manual_seed(1)).to(torch.int32)
-    pt = pages.view(B, maxp).to(dev)
-    kp = torch.zeros((B * maxp, S, Hkv, 128), dtype=torch.bfloat16, device=dev)
-    vp = torch.zeros_like(kp)
-    kn = torch.randn((B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
-    vn = torch.randn((B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
-    pos = torch.arange(B, dtype=torch.int32, device=dev) % (maxp * S)
-    us = burst(lambda: vd.vd_kv_append(kn, vn, kp, vp, pt, pos, stream=stream))
-    rows.append(dict(case="kv_append_B256", calls=iters, us_events=round(us, 2),
-                     algorithmic_bytes=2 * 2 * B * Hkv * 128 * 2 + B * 8))
+    if only is None:
+        B, Hkv, S, maxp = 256, 8, 16, 4
+        pages = torch.randperm(B * maxp, generator=torch.Generator().manual_seed(1)).to(torch.int32)
+        pt = pages.view(B, maxp).to(dev)
+        kp = torch.zeros((B * maxp, S, Hkv, 128), dtype=torch.bfloat16, device=dev)
+        vp = torch.zeros_like(kp)
+        kn = torch.randn((B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
+        vn = torch.randn((B, Hkv, 128), generator=gen, device=dev).to(torch.bfloat16)
+        pos = torch.arange(B, dtype=torch.int32, device=dev) % (maxp * S)
+        us = burst(lambda: vd.vd_kv_append(kn, vn, kp, vp, pt, pos, stream=stream))
+        rows.append(dict(case="kv_append_B256", calls=iters, us_events=round(us, 2),
+                         algorithmic_bytes=2 * 2 * B * Hkv * 128 * 2 + B * 8))
     os.makedirs(outdir, exist_ok=True)
     with open(os.path.join(outdir, "next_profile.csv"), "w") as f:
         f.write("case,calls,us_events,algorithmic_bytes\n")
@@ -818,6 +829,10 @@ def main():
     ap.add_argument("--next-profile", metavar="DIR", default=None,
                     help="short run of the GEMM (4 shapes x M 1/16/64/256/257/1024) and KV-append kernels "
                          "for a kernel trace; writes next_profile.csv to DIR")
+    ap.add_argument("--gemm-case", metavar="SHAPE:M", default=None,
+                    help="with --next-profile: only this GEMM case (e.g. gate_up:1024), no KV append")
+    ap.add_argument("--hipblaslt", action="store_true",
+                    help="with --gemm-case: run the case through torch.matmul (hipBLASLt) instead")
     ap.add_argument("--cpu-configs", metavar="DIR", default=None,
                     help="time the oracle on the host cores and the GPU on every seeded workload; "
                          "write oracle_cpu_baseline.{csv,json} to DIR")
@@ -870,7 +885,15 @@ def main():
         cpu_configs(args.cpu_configs)
         return
     if args.next_profile:
-        next_profile(args.next_profile)
+        only = None
+        if args.gemm_case:
+            shape, m = args.gemm_case.split(":")
+            if shape not in [g[0] for g in GEMM_SHAPES] or int(m) < 1:
+                raise SystemExit("--gemm-case: SHAPE:M with SHAPE one of %s" % [g[0] for g in GEMM_SHAPES])
+            only = (shape, int(m))
+        elif args.hipblaslt:
+            raise SystemExit("--hipblaslt needs --gemm-case")
+        next_profile(args.next_profile, only=only, hipblaslt=args.hipblaslt)
         if args.copy_calibration:
             n = args.copy_calibration // 4
             src = torch.ones(n, dtype=torch.int32, device="cuda:0")
