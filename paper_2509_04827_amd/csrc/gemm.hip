@@ -13,10 +13,11 @@
 //     x and w tiles of each K stage (BK columns) are loaded with 16-byte loads
 //     (whole 128- or 256-byte row pieces) into registers, and from there into
 //     one of two LDS buffers (rows padded by 16 bytes against bank
-//     conflicts), P stages ahead of the one being multiplied; the two
-//     largest tiles (128 x 128 and 256 x 128 for larger batches) load their
-//     stages straight from memory into a ring of LDS slots instead
-//     (gemm_dma_kernel), so the pipeline depth costs no registers;
+//     conflicts), P stages ahead of the one being multiplied; the tiles for
+//     larger batches (128 x 128 and 256 x 128 with four waves, 256 x 256 and
+//     192 x 256 with eight) load their stages straight from memory into a
+//     ring of LDS slots instead (gemm_dma_kernel), so the pipeline depth
+//     costs no registers;
 //   * each wave multiplies its (BN/WN) x (BM/WM) part of the tile with
 //     v_mfma_f32_16x16x32_bf16, the w fragment as the A operand (lane = output
 //     column) and the x fragment as B (lane = batch row), so the accumulator
@@ -247,15 +248,20 @@ __device__ inline void wait_vm_lds()
     __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
 }
 
-// Larger-batch tile with its stages loaded straight into LDS.  A stage is BK
-// columns (BK = 32 or 64: 64- or 128-byte rows of CH = BK / 8 chunks of 16
-// bytes) of the tile's BM x rows and BN w rows.  Each
-// global_load_lds_dwordx4 writes one 1 KiB block of LDS, lane l's 16 bytes
-// at the instruction's LDS base + 16 l, i.e. 64 / CH consecutive rows; lane
-// l loads row l / CH of the block and the chunk that puts row rho's chunk c
-// at slot c ^ swz(rho) (swz = rho mod 8 for 8 chunks, (rho / 2) mod 4 for
-// 4), so that the MFMA fragment reads (16 consecutive rows, one chunk) fall
-// in distinct banks.  NSLOT stages form a ring in LDS, up to NSLOT - 1 in
+// Larger-batch tile with its stages loaded straight into LDS, worked by
+// WM x WN waves (four, or eight: two per SIMD, 128 accumulators per lane for
+// a 256 x 256 tile, which a wave of four could only hold in AGPRs).  Per K
+// column the wide tiles move BM + BN operand rows for BM x BN products, so
+// 256 x 256 moves a third fewer rows per product than 256 x 128; with two
+// stages of 64 KiB in the ring it holds one workgroup per CU.  A stage is
+// BK = 64 columns (128-byte rows of CH = 8 chunks of 16 bytes) of the tile's
+// BM x rows and BN w rows.  Each global_load_lds_dwordx4 writes one 1 KiB
+// block of LDS, lane l's 16 bytes at the instruction's LDS base + 16 l, i.e.
+// 8 consecutive rows; lane l loads row l / 8 of the block and the chunk that
+// puts row rho's chunk c at slot c ^ (rho mod 8), so that the MFMA fragment
+// reads (16 consecutive rows, one chunk) fall in distinct banks.  The two
+// k-steps of 32 columns in a stage are its two halves.  NSLOT stages form a
+// ring in LDS, up to NSLOT - 1 in
 // flight while one is multiplied.  No registers carry the stages, so the
 // pipeline depth costs LDS only.  The waits are explicit: before stage k is
 // read, the wave waits for its own loads of stage k (the later stages' loads
@@ -264,27 +270,27 @@ __device__ inline void wait_vm_lds()
 // of stage k - 1 refilled.  Loads past the slice's end re-read its last
 // stage into a slot that is never read again, so every iteration issues the
 // same loads and the wait counts are constants.
-template <int CH>
 __device__ inline int chunk_swz(int row)
 {
-    return CH == 8 ? (row & 7) : ((row >> 1) & 3);
+    return row & 7;
 }
 
 template <int BM, int BN, int BK, int WM, int WN, int NSLOT, int MODE>
-__global__ void __launch_bounds__(kThreads)
+__global__ void __launch_bounds__(WM * WN * 64)
 gemm_dma_kernel(const GemmArgs a)
 {
+    constexpr int NW = WM * WN;                  // waves in the workgroup
     constexpr int CH = BK / 8;                   // 16-byte chunks per row
     constexpr int RPI = 64 / CH;                 // rows per load instruction
     constexpr int ROWS = BM + BN;                // x rows, then w rows, per stage
     constexpr int SLOT = ROWS * BK;              // bf16 elements per stage
-    constexpr int IPW = ROWS / RPI / 4;          // load instructions per wave and stage
+    constexpr int IPW = ROWS / RPI / NW;         // load instructions per wave and stage
     constexpr int H = BK / 32;                   // MFMA k-steps per stage
     constexpr int TM = BM / WM, TN = BN / WN;
     constexpr int FM = TM / 16, FN = TN / 16;
-    static_assert(BK == 32 || BK == 64, "stage width");
-    static_assert(WM * WN == kThreads / 64, "four waves");
-    static_assert(ROWS % (4 * RPI) == 0 && BM % RPI == 0 && TM % 16 == 0 && TN % 16 == 0, "shape");
+    static_assert(BK == 64, "stage width: two k-steps");
+    static_assert(NW == 4 || NW == 8, "four or eight waves");
+    static_assert(ROWS % (NW * RPI) == 0 && BM % RPI == 0 && TM % 16 == 0 && TN % 16 == 0, "shape");
     static_assert((NSLOT - 1) * IPW < 64, "vmcnt");
     __shared__ __attribute__((aligned(1024))) uint16_t lds[NSLOT * SLOT];
 
@@ -310,7 +316,7 @@ gemm_dma_kernel(const GemmArgs a)
     // this lane's source for each of its load instructions at stage 0; rows
     // past M repeat row M - 1 (loaded, never stored).  A block starts at a
     // multiple of RPI rows, so swz of the lane's row is swz(lane / CH).
-    const int chunk = (lane % CH) ^ chunk_swz<CH>(lane / CH);
+    const int chunk = (lane % CH) ^ chunk_swz(lane / CH);
     const uint16_t *src[IPW];
 #pragma unroll
     for (int j = 0; j < IPW; ++j) {
@@ -344,7 +350,7 @@ gemm_dma_kernel(const GemmArgs a)
     // the fragments of k-step h (32 columns: stage h / H, its half h % H)
     auto read = [&](Frags &f, int h) {
         const uint16_t *base = lds + ((h / H) % NSLOT) * SLOT;
-        const int sl = ((4 * (h % H) + kq) ^ chunk_swz<CH>(r)) * 8;   // this lane's chunk slot
+        const int sl = ((4 * (h % H) + kq) ^ chunk_swz(r)) * 8;   // this lane's chunk slot
 #pragma unroll
         for (int fn = 0; fn < FN; ++fn)
             f.a[fn] = *(const u32x4 *)(base + (BM + wn * TN + 16 * fn + r) * BK + sl);
@@ -386,7 +392,7 @@ gemm_dma_kernel(const GemmArgs a)
     asm volatile("" ::: "memory");
     Frags f0, f1;
     read(f0, 0);
-    for (int h = 0; h < nk * H; h += 2) {   // nk * H is even: K slices are whole 512 columns
+    for (int h = 0; h < nk * H; h += 2) {   // H is even: the pairs end on stage boundaries
         step(h, f0, f1);
         step(h + 1, f1, f0);
     }
@@ -444,22 +450,26 @@ gemm_reduce_kernel(const float *__restrict__ part, void *__restrict__ y, size_t 
 
 // ---------------------------------------------------------------- host side
 // The tile configurations (index = VD_GEMM_FLAG_TILE's argument), with the
-// two figures the automatic choice weighs them by, measured on MI355X: how
-// fast the tile streams weights relative to 5.482 TB/s once its workgroups
-// fill the device, and its matrix-core throughput (PFLOP/s) on a full device.
+// figures the automatic choice weighs them by: how many workgroups of the
+// tile a CU holds at once (its LDS and registers), and, measured on MI355X,
+// how fast the tile streams weights relative to 5.536 TB/s once its
+// workgroups fill the device and its matrix-core throughput (PFLOP/s) on a
+// full device.
 struct TileCfg {
-    int bm, bn, bk;
+    int bm, bn, bk, per_cu;
     double stream_eff, pflops;
 };
 constexpr TileCfg kTiles[] = {
-    {16, 64, 128, 1.167, 1.0},     // 0: four waves over the columns
-    {32, 64, 128, 1.2, 0.649},     // 1
-    {48, 64, 128, 0.746, 1.0},     // 2
-    {64, 64, 128, 0.714, 0.46},    // 3
-    {64, 128, 64, 0.991, 0.456},   // 4: 2 x 2 waves
-    {128, 128, 64, 0.853, 0.429},  // 5
-    {128, 128, 64, 1.2, 0.73},     // 6: stages loaded straight into LDS, four in a ring
-    {256, 128, 64, 0.908, 1.0},    // 7: the same, 2 x 2 waves of 128 x 64, three stages
+    {16, 64, 128, 3, 1.178, 0.59},    // 0: four waves over the columns
+    {32, 64, 128, 3, 1.3, 0.907},     // 1
+    {48, 64, 128, 2, 1.3, 1.386},     // 2
+    {64, 64, 128, 2, 0.681, 1.052},   // 3
+    {64, 128, 64, 2, 0.838, 0.445},   // 4: 2 x 2 waves
+    {128, 128, 64, 2, 0.981, 0.229},  // 5
+    {128, 128, 64, 1, 0.83, 0.798},   // 6: stages loaded straight into LDS, four in a ring
+    {256, 128, 64, 1, 1.195, 0.876},  // 7: the same, 2 x 2 waves of 128 x 64, three stages
+    {256, 256, 64, 1, 1.3, 1.272},    // 8: eight waves (2 x 4 of 128 x 64), two stages
+    {192, 256, 64, 1, 0.773, 1.309},  // 9: eight waves of 96 x 64, two stages
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
@@ -485,7 +495,9 @@ void launch_tile(int cfg, const GemmArgs &g, dim3 grid, hipStream_t stream)
             hipLaunchKernelGGL((gemm_tile_kernel<128, 128, 64, 2, 2, 2, MODE, false>), grid, block, 0, stream, g);
         break;
     case 6: hipLaunchKernelGGL((gemm_dma_kernel<128, 128, 64, 2, 2, 4, MODE>), grid, block, 0, stream, g); break;
-    default: hipLaunchKernelGGL((gemm_dma_kernel<256, 128, 64, 2, 2, 3, MODE>), grid, block, 0, stream, g); break;
+    case 7: hipLaunchKernelGGL((gemm_dma_kernel<256, 128, 64, 2, 2, 3, MODE>), grid, block, 0, stream, g); break;
+    case 8: hipLaunchKernelGGL((gemm_dma_kernel<256, 256, 64, 2, 4, 2, MODE>), grid, dim3(512), 0, stream, g); break;
+    default: hipLaunchKernelGGL((gemm_dma_kernel<192, 256, 64, 2, 4, 2, MODE>), grid, dim3(512), 0, stream, g); break;
     }
 }
 
@@ -529,30 +541,31 @@ long long plan_groups(const TileCfg &c, int M, int N, int S)
 }
 
 // Estimated time (microseconds) of a plan on MI355X: a fixed 4 us, plus the
-// larger of the weight stream (5.482 TB/s times the tile's streaming
+// larger of the weight stream (5.536 TB/s times the tile's streaming
 // efficiency, scaled down while its workgroups fill less than 192 CUs) and
 // the matrix-core time (the tile's throughput, scaled by the CUs it fills,
 // on the rows padded to whole tiles); K slices add the fp32 partials' round
-// trip at 2.648 TB/s and the reduction kernel (2.686 us); every 512
-// workgroups past the first 512 add 19.3 us.  The constants were fitted to a sweep of
-// every tile and 1, 2, 4 or 8 slices at the four Llama-3-8B-shaped
-// projections and 30 batch sizes M = 1 .. 1024, with weights that do not fit
-// the caches: the chosen plan costs 2.7% more than the best one on average.
+// trip at 3.59 TB/s and the reduction kernel (5 us); every round of
+// workgroups past the first (256 CUs times the tile's workgroups per CU)
+// adds 22.3 us.  The constants were fitted to a sweep of every tile and 1,
+// 2, 4 or 8 slices at the four Llama-3-8B-shaped projections and 30 batch
+// sizes M = 1 .. 1024, with weights that do not fit the caches: the chosen
+// plan costs 0.6% more than the best one on average and 8% in the worst case.
 double plan_cost(const TileCfg &c, int M, int N, int K, int S)
 {
     const double groups = (double)plan_groups(c, M, N, S);
     const double mpad = (double)((M + c.bm - 1) / c.bm) * c.bm;
-    const double t_w = (double)N * K * 2.0 / (5.482e6 * c.stream_eff * std::min(1.0, groups / 192.0));
+    const double t_w = (double)N * K * 2.0 / (5.536e6 * c.stream_eff * std::min(1.0, groups / 192.0));
     const double t_mfma = 2.0 * mpad * N * K / (c.pflops * 1e9 * std::min(1.0, groups / kTargetCUs));
-    const double t_part = S > 1 ? (double)S * M * N * 8.0 / 2.648e6 + 2.686 : 0.0;
-    const double waves = std::ceil(groups / 512.0);
-    return 4.0 + std::max(t_w, t_mfma) + t_part + 19.328 * (waves - 1.0);
+    const double t_part = S > 1 ? (double)S * M * N * 8.0 / 3.59e6 + 5.0 : 0.0;
+    const double rounds = std::ceil(groups / ((double)kTargetCUs * c.per_cu));
+    return 4.0 + std::max(t_w, t_mfma) + t_part + 22.312 * (rounds - 1.0);
 }
 
 // The automatic choice, from the sizes alone: the cheapest plan by
 // plan_cost over the tiles (for up to 64 rows, only the narrow tile that
 // holds the rows, 16 * ceil(M / 16), besides the wide ones) and 1, 2, 4 or 8
-// K slices of whole 512-column units.
+// K slices of whole stages of the tile.
 Plan auto_plan(int M, int N, int K)
 {
     Plan best{-1, 1};
@@ -564,7 +577,7 @@ Plan auto_plan(int M, int N, int K)
         if (t.bk == 128 && !(M <= 64 && t.bm == 16 * ((M + 15) / 16)))
             continue;
         for (int S = 1; S <= 8; S *= 2) {
-            if ((K / S) % kKAlign || K % S)
+            if (K % S || (K / S) % t.bk)
                 continue;
             const double cost = plan_cost(t, M, N, K, S);
             if (best.cfg < 0 || cost < best_cost) {

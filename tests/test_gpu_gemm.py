@@ -32,7 +32,12 @@ SHAPES = [(1, 4096, 4096), (7, 6144, 4096), (9, 4096, 4096), (16, 512, 512),
 
 # Every tile configuration with 1, 2, 8 and 16 K slices at two row counts
 # (37: several narrow row tiles; 300: a partial last tile of every size).
-FORCED = [(M, c, l) for M in (37, 300) for c in range(8) for l in (0, 1, 3, 4)]
+FORCED = [(M, c, l) for M in (37, 300) for c in range(10) for l in (0, 1, 3, 4)]
+
+# The LDS-fed tiles on many column tiles (2560 / BN of them, not a multiple of
+# the 8 XCDs, so both parts of the workgroup order are used) and a last row
+# tile that holds one row.
+WIDE = [(M, c, l) for M in (257, 513) for c in (6, 7, 8, 9) for l in (0, 1)]
 
 
 def inputs(M, N, K, seed):
@@ -85,6 +90,16 @@ def test_gemm_forced_tiles(M, cfg, slices_log2):
           flush=True)
     x, w = inputs(M, N, K, 7 * M + cfg)
     check(x, w, oracle.gemm(bits(x), bits(w)), flags, bf16=slices_log2 == 1)
+
+
+@pytest.mark.parametrize("M,cfg,slices_log2", WIDE)
+def test_gemm_forced_wide(M, cfg, slices_log2):
+    N, K = 2560, 1024
+    flags = vd.VD_GEMM_FLAG_TILE(cfg) | vd.VD_GEMM_FLAG_SLICES_LOG2(slices_log2)
+    print("case: gemm forced tile %d, %d slices, M %d N %d K %d" % (cfg, 1 << slices_log2, M, N, K),
+          flush=True)
+    x, w = inputs(M, N, K, 3 * M + cfg)
+    check(x, w, oracle.gemm(bits(x), bits(w)), flags, bf16=slices_log2 == 0)
 
 
 def test_gemm_deterministic():
