@@ -278,11 +278,11 @@ int vd_kv_append(const void *k_new, const void *v_new, void *k_pages,
  * VD_ERROR_NOT_SUPPORTED also for a forced tile or slice count that does not
  * fit the sizes.
  * Flags for tests and sweeps (0 = the automatic choice): VD_GEMM_FLAG_TILE(c)
- * forces tile configuration c (0..9: BM x BN = 16x64, 32x64, 48x64, 64x64,
- * 64x128, 128x128, and four tiles whose K stages go straight from memory into
- * LDS, 128x128, 256x128, 256x256 and 192x256; BM rows of x, BN of w; BN = 128
- * needs N % 128 == 0, BN = 256 needs N % 256 == 0), VD_GEMM_FLAG_SLICES_LOG2(l)
- * forces 2^l K slices (l <= 4).
+ * forces tile configuration c (0..10: BM x BN = 16x64, 32x64, 48x64, 64x64,
+ * 64x128, 128x128, and five tiles whose K stages go straight from memory into
+ * LDS, 128x128, 256x128, 256x256, 192x256 and 320x256; BM rows of x, BN of w;
+ * BN = 128 needs N % 128 == 0, BN = 256 needs N % 256 == 0),
+ * VD_GEMM_FLAG_SLICES_LOG2(l) forces 2^l K slices (l <= 4).
  * These bits mean something else for the attention calls.
  */
 #define VD_GEMM_FLAG_TILE_SHIFT 8u

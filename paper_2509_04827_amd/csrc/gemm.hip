@@ -14,8 +14,8 @@
 //     (whole 128- or 256-byte row pieces) into registers, and from there into
 //     one of two LDS buffers (rows padded by 16 bytes against bank
 //     conflicts), P stages ahead of the one being multiplied; the tiles for
-//     larger batches (128 x 128 and 256 x 128 with four waves, 256 x 256 and
-//     192 x 256 with eight) load their stages straight from memory into a
+//     larger batches (128 x 128 and 256 x 128 with four waves; 192, 256 or
+//     320 x 256 with eight) load their stages straight from memory into a
 //     ring of LDS slots instead (gemm_dma_kernel), so the pipeline depth
 //     costs no registers;
 //   * each wave multiplies its (BN/WN) x (BM/WM) part of the tile with
@@ -250,7 +250,8 @@ __device__ inline void wait_vm_lds()
 
 // Larger-batch tile with its stages loaded straight into LDS, worked by
 // WM x WN waves (four, or eight: two per SIMD, 128 accumulators per lane for
-// a 256 x 256 tile, which a wave of four could only hold in AGPRs).  Per K
+// a 256 x 256 tile, 160 for 320 x 256, which waves of four could only hold
+// in AGPRs).  Per K
 // column the wide tiles move BM + BN operand rows for BM x BN products, so
 // 256 x 256 moves a third fewer rows per product than 256 x 128; with two
 // stages of 64 KiB in the ring it holds one workgroup per CU.  A stage is
@@ -452,7 +453,7 @@ gemm_reduce_kernel(const float *__restrict__ part, void *__restrict__ y, size_t 
 // The tile configurations (index = VD_GEMM_FLAG_TILE's argument), with the
 // figures the automatic choice weighs them by: how many workgroups of the
 // tile a CU holds at once (its LDS and registers), and, measured on MI355X,
-// how fast the tile streams weights relative to 5.536 TB/s once its
+// how fast the tile streams weights relative to 5.623 TB/s once its
 // workgroups fill the device and its matrix-core throughput (PFLOP/s) on a
 // full device.
 struct TileCfg {
@@ -460,16 +461,17 @@ struct TileCfg {
     double stream_eff, pflops;
 };
 constexpr TileCfg kTiles[] = {
-    {16, 64, 128, 3, 1.178, 0.59},    // 0: four waves over the columns
-    {32, 64, 128, 3, 1.3, 0.907},     // 1
-    {48, 64, 128, 2, 1.3, 1.386},     // 2
-    {64, 64, 128, 2, 0.681, 1.052},   // 3
-    {64, 128, 64, 2, 0.838, 0.445},   // 4: 2 x 2 waves
-    {128, 128, 64, 2, 0.981, 0.229},  // 5
-    {128, 128, 64, 1, 0.83, 0.798},   // 6: stages loaded straight into LDS, four in a ring
-    {256, 128, 64, 1, 1.195, 0.876},  // 7: the same, 2 x 2 waves of 128 x 64, three stages
-    {256, 256, 64, 1, 1.3, 1.272},    // 8: eight waves (2 x 4 of 128 x 64), two stages
-    {192, 256, 64, 1, 0.773, 1.309},  // 9: eight waves of 96 x 64, two stages
+    {16, 64, 128, 3, 1.121, 1.0},     // 0: four waves over the columns
+    {32, 64, 128, 3, 1.3, 1.073},     // 1
+    {48, 64, 128, 2, 1.182, 1.6},     // 2
+    {64, 64, 128, 2, 0.897, 1.222},   // 3
+    {64, 128, 64, 2, 0.977, 0.56},    // 4: 2 x 2 waves
+    {128, 128, 64, 2, 1.3, 0.309},    // 5
+    {128, 128, 64, 1, 0.854, 1.004},  // 6: stages loaded straight into LDS, four in a ring
+    {256, 128, 64, 1, 1.3, 0.993},    // 7: the same, 2 x 2 waves of 128 x 64, three stages
+    {256, 256, 64, 1, 0.511, 1.421},  // 8: eight waves (2 x 4 of 128 x 64), two stages
+    {192, 256, 64, 1, 0.658, 1.132},  // 9: eight waves of 96 x 64, two stages
+    {320, 256, 64, 1, 0.925, 1.267},  // 10: eight waves of 160 x 64, two stages
 };
 constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 
@@ -497,7 +499,8 @@ void launch_tile(int cfg, const GemmArgs &g, dim3 grid, hipStream_t stream)
     case 6: hipLaunchKernelGGL((gemm_dma_kernel<128, 128, 64, 2, 2, 4, MODE>), grid, block, 0, stream, g); break;
     case 7: hipLaunchKernelGGL((gemm_dma_kernel<256, 128, 64, 2, 2, 3, MODE>), grid, block, 0, stream, g); break;
     case 8: hipLaunchKernelGGL((gemm_dma_kernel<256, 256, 64, 2, 4, 2, MODE>), grid, dim3(512), 0, stream, g); break;
-    default: hipLaunchKernelGGL((gemm_dma_kernel<192, 256, 64, 2, 4, 2, MODE>), grid, dim3(512), 0, stream, g); break;
+    case 9: hipLaunchKernelGGL((gemm_dma_kernel<192, 256, 64, 2, 4, 2, MODE>), grid, dim3(512), 0, stream, g); break;
+    default: hipLaunchKernelGGL((gemm_dma_kernel<320, 256, 64, 2, 4, 2, MODE>), grid, dim3(512), 0, stream, g); break;
     }
 }
 
@@ -541,25 +544,25 @@ long long plan_groups(const TileCfg &c, int M, int N, int S)
 }
 
 // Estimated time (microseconds) of a plan on MI355X: a fixed 4 us, plus the
-// larger of the weight stream (5.536 TB/s times the tile's streaming
+// larger of the weight stream (5.623 TB/s times the tile's streaming
 // efficiency, scaled down while its workgroups fill less than 192 CUs) and
 // the matrix-core time (the tile's throughput, scaled by the CUs it fills,
 // on the rows padded to whole tiles); K slices add the fp32 partials' round
-// trip at 3.59 TB/s and the reduction kernel (5 us); every round of
+// trip at 8 TB/s and the reduction kernel (1.8 us); every round of
 // workgroups past the first (256 CUs times the tile's workgroups per CU)
-// adds 22.3 us.  The constants were fitted to a sweep of every tile and 1,
+// adds 23.3 us.  The constants were fitted to a sweep of every tile and 1,
 // 2, 4 or 8 slices at the four Llama-3-8B-shaped projections and 30 batch
 // sizes M = 1 .. 1024, with weights that do not fit the caches: the chosen
-// plan costs 0.6% more than the best one on average and 8% in the worst case.
+// plan costs 0.55% more than the best one on average and 8% in the worst case.
 double plan_cost(const TileCfg &c, int M, int N, int K, int S)
 {
     const double groups = (double)plan_groups(c, M, N, S);
     const double mpad = (double)((M + c.bm - 1) / c.bm) * c.bm;
-    const double t_w = (double)N * K * 2.0 / (5.536e6 * c.stream_eff * std::min(1.0, groups / 192.0));
+    const double t_w = (double)N * K * 2.0 / (5.623e6 * c.stream_eff * std::min(1.0, groups / 192.0));
     const double t_mfma = 2.0 * mpad * N * K / (c.pflops * 1e9 * std::min(1.0, groups / kTargetCUs));
-    const double t_part = S > 1 ? (double)S * M * N * 8.0 / 3.59e6 + 5.0 : 0.0;
+    const double t_part = S > 1 ? (double)S * M * N * 8.0 / 8.0e6 + 1.824 : 0.0;
     const double rounds = std::ceil(groups / ((double)kTargetCUs * c.per_cu));
-    return 4.0 + std::max(t_w, t_mfma) + t_part + 22.312 * (rounds - 1.0);
+    return 4.0 + std::max(t_w, t_mfma) + t_part + 23.255 * (rounds - 1.0);
 }
 
 // The automatic choice, from the sizes alone: the cheapest plan by

@@ -171,12 +171,13 @@ def test_gemm_argument_errors():
     assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_SLICES_LOG2(0)) == 0
     assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_SLICES_LOG2(3)) == 8 * 64 * 4096 * 4
     assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_TILE(5) | vd.VD_GEMM_FLAG_SLICES_LOG2(4)) == 16 * 64 * 4096 * 4
-    assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_TILE(10)) == 0   # no such tile
+    assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_TILE(11)) == 0   # no such tile
     assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_TILE(7) | vd.VD_GEMM_FLAG_SLICES_LOG2(0)) == 0
     assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_TILE(9) | vd.VD_GEMM_FLAG_SLICES_LOG2(1)) == 2 * 64 * 4096 * 4
     assert ws(4, 192, 512, vd.VD_GEMM_FLAG_TILE(6)) == 0       # 128-column LDS-fed tile, N % 128
     assert ws(4, 384, 512, vd.VD_GEMM_FLAG_TILE(8)) == 0       # 256-column tile, N % 256
     assert ws(4, 384, 512, vd.VD_GEMM_FLAG_TILE(9)) == 0
+    assert ws(4, 384, 512, vd.VD_GEMM_FLAG_TILE(10)) == 0
     assert ws(64, 4096, 4096, vd.VD_GEMM_FLAG_SLICES_LOG2(5)) == 0   # 32 slices
     assert ws(4, 4096, 512, vd.VD_GEMM_FLAG_SLICES_LOG2(3)) == 0     # 64-column slices: not whole 128-column stages
     assert ws(4, 192, 512, vd.VD_GEMM_FLAG_TILE(4)) == 0       # 128-column tile, N % 128

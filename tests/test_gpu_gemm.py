@@ -32,12 +32,12 @@ SHAPES = [(1, 4096, 4096), (7, 6144, 4096), (9, 4096, 4096), (16, 512, 512),
 
 # Every tile configuration with 1, 2, 8 and 16 K slices at two row counts
 # (37: several narrow row tiles; 300: a partial last tile of every size).
-FORCED = [(M, c, l) for M in (37, 300) for c in range(10) for l in (0, 1, 3, 4)]
+FORCED = [(M, c, l) for M in (37, 300) for c in range(11) for l in (0, 1, 3, 4)]
 
 # The LDS-fed tiles on many column tiles (2560 / BN of them, not a multiple of
 # the 8 XCDs, so both parts of the workgroup order are used) and a last row
 # tile that holds one row.
-WIDE = [(M, c, l) for M in (257, 513) for c in (6, 7, 8, 9) for l in (0, 1)]
+WIDE = [(M, c, l) for M in (257, 513) for c in (6, 7, 8, 9, 10) for l in (0, 1)]
 
 
 def inputs(M, N, K, seed):
