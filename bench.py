@@ -491,9 +491,15 @@ def gemm_sweep(outdir: str, iters: int = 20, warmup: int = 3):
 LAYER_BATCH = (1, 4, 16, 32, 64, 128, 192, 256, 384, 512)
 LAYER_LEN = (16, 64, 256, 1024, 4096)
 LAYER_RING = 4
+# the dense batch grid: both sides of the projection GEMMs' row-tile steps
+# (128 -> 160, 256 -> 257, 512 -> 513) at three lengths, layer time only
+LAYER_DENSE_BATCH = (1, 32, 64, 96, 128, 144, 160, 192, 224, 240, 248, 255, 256, 257, 264, 272,
+                     288, 320, 384, 448, 480, 496, 504, 511, 512, 513, 520, 528, 544, 576, 640)
+LAYER_DENSE_LEN = (64, 256, 1024)
 
 
-def layer_surface(outdir: str, reps: int = 5):
+def layer_surface(outdir: str, reps: int = 5, batches=LAYER_BATCH, lengths=LAYER_LEN,
+                  components: bool = True, name: str = "decode_layer_surface"):
     """Time of one decode layer step built from this library's kernels over
     (N_req, tokens per request): the decode iteration the paper's latency
     model predicts (Sec. 5.4, Eq. pred-itl), whose N_req term the projection
@@ -509,7 +515,8 @@ def layer_surface(outdir: str, reps: int = 5):
     iteration.  Each point: the four layers captured into one HIP graph
     (kernel launches only), replayed `reps` times after a warm-up replay and
     20 ms of untimed replays; per-component graphs of the same four layers
-    give the split.  Fits T = c*N_req + d*N_kv + e and the boosted model."""
+    give the split (`components`).  Fits T = c*N_req + d*N_kv + e, the same
+    form per GEMM tile region, and the boosted model."""
     import numpy as np
     import torch
 
@@ -527,8 +534,8 @@ def layer_surface(outdir: str, reps: int = 5):
         return torch.randn(shape, generator=gen, device=dev).to(torch.bfloat16)
 
     weights = [{k: rnd(n, kk) for k, (n, kk) in shapes.items()} for _ in range(LAYER_RING)]
-    max_tok = max(b * l for b in LAYER_BATCH for l in LAYER_LEN)
-    pages_per_layer = max_tok // S + max(LAYER_BATCH)
+    max_tok = max(b * l for b in batches for l in lengths)
+    pages_per_layer = max_tok // S + max(batches)
     npages = pages_per_layer * LAYER_RING
     kpool = torch.empty((npages, S, Hkv, D), dtype=torch.bfloat16, device=dev)
     vpool = torch.empty_like(kpool)
@@ -539,7 +546,7 @@ def layer_surface(outdir: str, reps: int = 5):
     scale = float(np.float32(1.0 / np.sqrt(D)))
     rows = []
 
-    for B in LAYER_BATCH:
+    for B in batches:
         x = rnd(B, H)
         y_qkv = torch.empty((B, 6144), dtype=torch.bfloat16, device=dev)
         q = rnd(B, Hq, D)
@@ -551,7 +558,7 @@ def layer_surface(outdir: str, reps: int = 5):
         y_down = torch.empty((B, H), dtype=torch.bfloat16, device=dev)
         gws = {k: torch.empty(max(16, vd.vd_gemm_workspace_size(B, n, kk)), dtype=torch.uint8, device=dev)
                for k, (n, kk) in shapes.items()}
-        for L in LAYER_LEN:
+        for L in lengths:
             if B * L > max_tok:
                 continue
             P = (L + S - 1) // S
@@ -599,16 +606,18 @@ def layer_surface(outdir: str, reps: int = 5):
 
             row = dict(n_req=B, tokens_per_req=L, n_kv=B * L)
             row["us_layer"] = round(graph_us(list(comps)), 2)
-            for n in comps:
-                row["us_" + n] = round(graph_us([n]), 2)
+            if components:
+                for n in comps:
+                    row["us_" + n] = round(graph_us([n]), 2)
             rows.append(row)
-            print("layer B %4d L %5d N_kv %8d  layer %8.2f us  (qkv %.1f append %.1f attn %.1f o %.1f gu %.1f down %.1f)"
-                  % (B, L, B * L, row["us_layer"], row["us_qkv"], row["us_append"], row["us_attn"],
-                     row["us_o_proj"], row["us_gate_up"], row["us_down"]), file=sys.stderr, flush=True)
+            print("layer B %4d L %5d N_kv %8d  layer %8.2f us  %s"
+                  % (B, L, B * L, row["us_layer"], " ".join("%s %.1f" % (k[3:], v) for k, v in row.items()
+                                                            if k.startswith("us_") and k != "us_layer")),
+                  file=sys.stderr, flush=True)
             del aws, pts
     os.makedirs(outdir, exist_ok=True)
     keys = list(rows[0].keys())
-    with open(os.path.join(outdir, "decode_layer_surface.csv"), "w") as f:
+    with open(os.path.join(outdir, name + ".csv"), "w") as f:
         f.write(",".join(keys) + "\n")
         for r in rows:
             f.write(",".join(str(r[k]) for k in keys) + "\n")
@@ -616,9 +625,14 @@ def layer_surface(outdir: str, reps: int = 5):
     n_kv = np.array([r["n_kv"] for r in rows], float)
     t = np.array([r["us_layer"] for r in rows], float)
     fit = lm.fit_linear(n_req, n_kv, t)
+    bounds = (256, 512)
+    tf = lm.fit_per_tile(n_req, n_kv, t, bounds)
     res = {"points": len(rows), "c_us_per_req": fit.c, "d_us_per_kv_token": fit.d, "e_us": fit.e,
-           "r2": fit.r2, "mae_us": fit.mae, "holdout": lm.holdout_mae(n_req, n_kv, t)}
-    with open(os.path.join(outdir, "decode_layer_surface_fit.json"), "w") as f:
+           "r2": fit.r2, "mae_us": fit.mae,
+           "per_tile": [{"n_req_max": b, "c": f.c, "d": f.d, "e": f.e, "r2": f.r2, "mae_us": f.mae}
+                        for b, f in zip(list(bounds) + [None], tf.fits)],
+           "holdout": lm.holdout_mae(n_req, n_kv, t, tile_bounds=bounds)}
+    with open(os.path.join(outdir, name + "_fit.json"), "w") as f:
         json.dump(res, f, indent=1)
     print(json.dumps(res), flush=True)
 
@@ -836,6 +850,9 @@ def main():
     ap.add_argument("--cpu-configs", metavar="DIR", default=None,
                     help="time the oracle on the host cores and the GPU on every seeded workload; "
                          "write oracle_cpu_baseline.{csv,json} to DIR")
+    ap.add_argument("--layer-dense", metavar="DIR", default=None,
+                    help="instead of the bench line, time the decode layer step over a dense batch grid "
+                         "around the GEMM tile steps and write DIR/decode_layer_dense.csv")
     ap.add_argument("--layer-surface", metavar="DIR", default=None,
                     help="instead of the bench line, time a decode layer step (qkv GEMM, KV append, "
                          "attention, o_proj / gate_up / down GEMMs) over (batch, tokens per request) "
@@ -874,6 +891,10 @@ def main():
         return
     if args.layer_surface:
         layer_surface(args.layer_surface)
+        return
+    if args.layer_dense:
+        layer_surface(args.layer_dense, batches=LAYER_DENSE_BATCH, lengths=LAYER_DENSE_LEN,
+                      components=False, name="decode_layer_dense")
         return
     if args.gemm_sweep:
         gemm_sweep(args.gemm_sweep)

@@ -99,6 +99,42 @@ def fit_linear(n_req, n_kv, t) -> LinearFit:
                      float(np.abs(t - pred).mean()))
 
 
+@dataclass
+class TileFit:
+    """Eq. pred-itl within each GEMM tile (Sec. 5.4): one (c, d, e) per band
+    of N_req between the batch sizes where the projection GEMMs need another
+    row tile (Sec. 3.3).  Band i holds bounds[i-1] < N_req <= bounds[i]; the
+    last band is open above."""
+    bounds: tuple
+    fits: list
+
+    def band(self, n_req):
+        return np.searchsorted(np.asarray(self.bounds, float), np.asarray(n_req, float), side="left")
+
+    def predict(self, n_req, n_kv):
+        n_req, n_kv = np.asarray(n_req, float), np.asarray(n_kv, float)
+        b = self.band(n_req)
+        out = np.empty(n_req.shape, float)
+        for i, f in enumerate(self.fits):
+            sel = b == i
+            out[sel] = f.predict(n_req[sel], n_kv[sel])
+        return out
+
+
+def fit_per_tile(n_req, n_kv, t, bounds=(256, 512)) -> TileFit:
+    """Eq. pred-itl fitted separately in each band of N_req (see TileFit);
+    every band needs points of its own."""
+    n_req, n_kv, t = (np.asarray(x, float) for x in (n_req, n_kv, t))
+    b = np.searchsorted(np.asarray(bounds, float), n_req, side="left")
+    fits = []
+    for i in range(len(bounds) + 1):
+        sel = b == i
+        if sel.sum() < 3:
+            raise ValueError("band %d of N_req has %d points; the fit needs 3" % (i, int(sel.sum())))
+        fits.append(fit_linear(n_req[sel], n_kv[sel], t[sel]))
+    return TileFit(tuple(bounds), fits)
+
+
 def fit_boosted(n_req, n_kv, t, random_state: int = 42):
     """Boosted trees on (n_req, n_kv) with the decode settings of the paper."""
     from sklearn.ensemble import HistGradientBoostingRegressor
@@ -112,8 +148,10 @@ def fit_boosted(n_req, n_kv, t, random_state: int = 42):
     return model
 
 
-def holdout_mae(n_req, n_kv, t, test_fraction: float = 0.25, seed: int = 0):
-    """MAE of both models on a random held-out share of the points."""
+def holdout_mae(n_req, n_kv, t, test_fraction: float = 0.25, seed: int = 0, tile_bounds=None):
+    """MAE of the models on a random held-out share of the points: the
+    linear form over all points, the boosted trees and, with `tile_bounds`,
+    the linear form per tile band."""
     n_req, n_kv, t = (np.asarray(x, float) for x in (n_req, n_kv, t))
     rng = np.random.default_rng(seed)
     idx = rng.permutation(t.shape[0])
@@ -123,5 +161,9 @@ def holdout_mae(n_req, n_kv, t, test_fraction: float = 0.25, seed: int = 0):
     gb = fit_boosted(n_req[tr], n_kv[tr], t[tr])
     lin_mae = float(np.abs(lin.predict(n_req[te], n_kv[te]) - t[te]).mean())
     gb_mae = float(np.abs(gb.predict(np.stack([n_req[te], n_kv[te]], 1)) - t[te]).mean())
-    return {"linear_mae_us": lin_mae, "boosted_mae_us": gb_mae, "n_train": int(tr.size),
-            "n_test": int(te.size)}
+    out = {"linear_mae_us": lin_mae, "boosted_mae_us": gb_mae, "n_train": int(tr.size),
+           "n_test": int(te.size)}
+    if tile_bounds is not None:
+        tf = fit_per_tile(n_req[tr], n_kv[tr], t[tr], tile_bounds)
+        out["tile_linear_mae_us"] = float(np.abs(tf.predict(n_req[te], n_kv[te]) - t[te]).mean())
+    return out

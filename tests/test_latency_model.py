@@ -117,3 +117,43 @@ def test_committed_layer_surface_charges_requests_to_the_gemms():
     # one component at a time adds in gaps
     parts = gemm + attn + np.array([float(r["us_append"]) for r in rows])
     assert np.all(np.abs(parts - t) < 0.15 * t + 10)
+
+
+def test_per_tile_fit_follows_a_staircase():
+    """Eq. pred-itl within each tile (Sec. 5.4): a surface with steps at the
+    tile boundaries is exact per band, and one plane over all bands is not."""
+    import pytest
+    n_req = np.repeat([1, 32, 64, 128, 192, 255, 256, 257, 300, 384, 448, 512, 513, 576, 640], 3).astype(float)
+    n_kv = n_req * np.tile([64, 256, 1024], 15)
+    t = 0.4 * n_req + 6e-4 * n_kv + 100 + 20 * (n_req > 256) + 30 * (n_req > 512)
+    tf = lm.fit_per_tile(n_req, n_kv, t, (256, 512))
+    assert np.abs(tf.predict(n_req, n_kv) - t).max() < 1e-6
+    assert list(tf.band([1, 256, 257, 512, 513, 10 ** 6])) == [0, 0, 1, 1, 2, 2]
+    assert lm.fit_linear(n_req, n_kv, t).mae > 5
+    with pytest.raises(ValueError):
+        lm.fit_per_tile(n_req[n_req <= 300], n_kv[n_req <= 300], t[n_req <= 300], (256, 512))
+
+
+def test_committed_dense_surface_shows_the_tile_steps():
+    """The decode layer step measured on a dense batch grid (profiles/): it
+    jumps where the projection GEMMs need another row tile (Sec. 3.3,
+    256 -> 257 and 512 -> 513) at every length, and Eq. pred-itl fitted per
+    band between those boundaries predicts held-out points with well under
+    half the error of one plane over all of them."""
+    import csv
+    import os
+    path = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                        "profiles", "decode_layer_dense.csv")
+    rows = list(csv.DictReader(open(path)))
+    assert len(rows) >= 80
+    for L in {r["tokens_per_req"] for r in rows}:
+        v = {int(r["n_req"]): float(r["us_layer"]) for r in rows if r["tokens_per_req"] == L}
+        assert v[257] > 1.05 * v[256] and v[513] > 1.05 * v[512]
+        assert v[256] <= 1.02 * v[255] and v[512] <= 1.02 * v[511]   # no step before the boundary
+    n_req, n_kv, t = lm.load_surface(path, n_q_heads=None, column="us_layer")
+    tf = lm.fit_per_tile(n_req, n_kv, t, (256, 512))
+    assert min(f.r2 for f in tf.fits) > 0.97
+    ho = [lm.holdout_mae(n_req, n_kv, t, seed=s, tile_bounds=(256, 512)) for s in range(5)]
+    tile = np.mean([h["tile_linear_mae_us"] for h in ho])
+    lin = np.mean([h["linear_mae_us"] for h in ho])
+    assert tile < 0.5 * lin
