@@ -55,7 +55,7 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kThreads = 256;                 // four waves per workgroup
+constexpr int kThreads = 256;                 // four waves per workgroup (eight for the 256-column tiles)
 constexpr int kNAlign = 64;                   // N granularity
 constexpr int kKAlign = 512;                  // K granularity
 constexpr int kReduceThreads = 256;
@@ -478,7 +478,7 @@ constexpr int kNumTiles = (int)(sizeof(kTiles) / sizeof(kTiles[0]));
 template <int MODE>
 void launch_tile(int cfg, const GemmArgs &g, dim3 grid, hipStream_t stream)
 {
-    const dim3 block(kThreads);
+    const dim3 block(kThreads), block8(2 * kThreads);
     switch (cfg) {
     case 0: hipLaunchKernelGGL((gemm_tile_kernel<16, 64, 128, 1, 4, 4, MODE>), grid, block, 0, stream, g); break;
     case 1: hipLaunchKernelGGL((gemm_tile_kernel<32, 64, 128, 1, 4, 3, MODE>), grid, block, 0, stream, g); break;
@@ -498,9 +498,9 @@ void launch_tile(int cfg, const GemmArgs &g, dim3 grid, hipStream_t stream)
         break;
     case 6: hipLaunchKernelGGL((gemm_dma_kernel<128, 128, 64, 2, 2, 4, MODE>), grid, block, 0, stream, g); break;
     case 7: hipLaunchKernelGGL((gemm_dma_kernel<256, 128, 64, 2, 2, 3, MODE>), grid, block, 0, stream, g); break;
-    case 8: hipLaunchKernelGGL((gemm_dma_kernel<256, 256, 64, 2, 4, 2, MODE>), grid, dim3(512), 0, stream, g); break;
-    case 9: hipLaunchKernelGGL((gemm_dma_kernel<192, 256, 64, 2, 4, 2, MODE>), grid, dim3(512), 0, stream, g); break;
-    default: hipLaunchKernelGGL((gemm_dma_kernel<320, 256, 64, 2, 4, 2, MODE>), grid, dim3(512), 0, stream, g); break;
+    case 8: hipLaunchKernelGGL((gemm_dma_kernel<256, 256, 64, 2, 4, 2, MODE>), grid, block8, 0, stream, g); break;
+    case 9: hipLaunchKernelGGL((gemm_dma_kernel<192, 256, 64, 2, 4, 2, MODE>), grid, block8, 0, stream, g); break;
+    default: hipLaunchKernelGGL((gemm_dma_kernel<320, 256, 64, 2, 4, 2, MODE>), grid, block8, 0, stream, g); break;
     }
 }
 
