@@ -7,7 +7,7 @@
 // at batch 256 -> 257 to GEMM tile quantisation (Sec. 3.3).  Up to a few
 // hundred rows the GEMM is bound by reading the weights (2*M flop per weight
 // element against ~312 flop/B of MFMA-to-HBM balance); past that, by the
-// matrix cores.  One tiled kernel covers both:
+// matrix cores.  Two tiled kernels cover both, under one plan:
 //
 //   * a workgroup of four waves owns a BM x BN output tile and a K slice; the
 //     x and w tiles of each K stage (BK columns) are loaded with 16-byte loads
@@ -34,8 +34,9 @@
 //     workgroups; each slice writes an fp32 partial and a second kernel adds
 //     the slices in order (deterministic, no atomics).
 //
-// The tile shape and S follow from (M, N, K) alone (a table tuned on MI355X),
-// so the result and the workspace size do not depend on the device.
+// The tile shape and S follow from (M, N, K) alone (a cost model whose
+// constants were fitted on MI355X), so the result and the workspace size do
+// not depend on the device.
 //
 // x bf16 [M][K], w bf16 [N][K] (a linear layer's weight), y bf16 (RNE) or
 // fp32 [M][N]; fp32 accumulation.
