@@ -20,15 +20,18 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 
 # Automatic plans over the decode range: the narrow 16-64-row tiles with 1-4
-# K slices, the 64x128 and 128x128 tiles with and without slices, rows that
-# are not whole tiles, and the batch-size steps of the paper's tile
-# quantisation (255/256/257, 512/513) up to 1024 rows.
+# K slices, the 64x128 and 128x128 tiles with and without slices, the larger
+# LDS-fed tiles, rows that are not whole tiles, and the batch-size steps of
+# the paper's tile quantisation (255/256/257, 512/513) up to 1024 rows.
 SHAPES = [(1, 4096, 4096), (7, 6144, 4096), (9, 4096, 4096), (16, 512, 512),
           (33, 1024, 14336), (48, 4096, 14336), (64, 28672, 4096), (64, 64, 512), (17, 128, 1024),
           (3, 4096, 14336), (4, 2048, 2048),
           (96, 4096, 4096), (128, 6144, 4096), (192, 2048, 14336), (255, 4096, 4096),
           (256, 4096, 4096), (257, 4096, 4096), (512, 2048, 2048), (513, 2048, 4096),
-          (1024, 1024, 2048), (1024, 4096, 1024)]
+          (1024, 1024, 2048), (1024, 4096, 1024),
+          # shapes whose automatic plan takes each of the larger LDS-fed tiles
+          # (256x128, 192x256, 256x256, 320x256)
+          (257, 16384, 512), (257, 28672, 512), (1024, 12288, 512), (513, 28672, 512)]
 
 # Every tile configuration with 1, 2, 8 and 16 K slices at two row counts
 # (37: several narrow row tiles; 300: a partial last tile of every size).
