@@ -42,6 +42,11 @@ FORCED = [(M, c, l) for M in (37, 300) for c in range(11) for l in (0, 1, 3, 4)]
 # tile that holds one row.
 WIDE = [(M, c, l) for M in (257, 513) for c in (6, 7, 8, 9, 10) for l in (0, 1)]
 
+# The 64-column-stage tiles on K slices of one and two stages (K = 512 in 8
+# or 4 slices): the shortest pipelines, where the ring's loads past the end
+# and the first stage's wait meet.
+SHORT_K = [(M, c, l) for M in (37, 300) for c in (4, 5, 6, 7, 8, 9, 10) for l in (2, 3)]
+
 
 def inputs(M, N, K, seed):
     g = torch.Generator().manual_seed(seed)
@@ -103,6 +108,16 @@ def test_gemm_forced_wide(M, cfg, slices_log2):
           flush=True)
     x, w = inputs(M, N, K, 3 * M + cfg)
     check(x, w, oracle.gemm(bits(x), bits(w)), flags, bf16=slices_log2 == 0)
+
+
+@pytest.mark.parametrize("M,cfg,slices_log2", SHORT_K)
+def test_gemm_forced_short_slices(M, cfg, slices_log2):
+    N, K = 512, 512
+    flags = vd.VD_GEMM_FLAG_TILE(cfg) | vd.VD_GEMM_FLAG_SLICES_LOG2(slices_log2)
+    print("case: gemm forced tile %d, %d slices, M %d N %d K %d" % (cfg, 1 << slices_log2, M, N, K),
+          flush=True)
+    x, w = inputs(M, N, K, 5 * M + cfg)
+    check(x, w, oracle.gemm(bits(x), bits(w)), flags, bf16=False)
 
 
 def test_gemm_deterministic():
