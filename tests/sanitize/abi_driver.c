@@ -64,6 +64,29 @@ int main(void)
     CHECK(vd_gemm_bf16(NULL, F, F, 1, 64, 512, F, 1 << 20, 0, NULL) == VD_ERROR_INVALID_VALUE, "gemm null");
     CHECK(vd_stream_read(NULL, 1024, F, 8, NULL) == VD_ERROR_INVALID_VALUE, "stream null");
 
+    /* the GEMM plan over sizes and every forced tile and slice count
+     * (including ones past the table): a workspace is 0 or S fp32 partials
+     * of M x N with S a power of two up to 16 */
+    {
+        const int Ms[] = {1, 7, 16, 17, 63, 64, 65, 255, 256, 257, 513, 640, 1024, 4096, 1 << 16};
+        const int Ns[] = {64, 128, 192, 256, 4096, 6144, 28672, 1 << 20};
+        const int Ks[] = {512, 1024, 4096, 14336, 1 << 20};
+        for (size_t a = 0; a < sizeof(Ms) / sizeof(Ms[0]); ++a)
+            for (size_t b = 0; b < sizeof(Ns) / sizeof(Ns[0]); ++b)
+                for (size_t c = 0; c < sizeof(Ks) / sizeof(Ks[0]); ++c)
+                    for (int t = -1; t < 16; ++t)
+                        for (int l = -1; l < 16; l += 3) {
+                            const unsigned fl = (t >= 0 ? VD_GEMM_FLAG_TILE(t) : 0u) |
+                                                (l >= 0 ? VD_GEMM_FLAG_SLICES_LOG2(l) : 0u);
+                            const size_t n = vd_gemm_workspace_size(Ms[a], Ns[b], Ks[c], fl);
+                            const size_t unit = (size_t)Ms[a] * Ns[b] * 4;
+                            int ok = n == 0;
+                            for (int S = 2; S <= 16 && !ok; S *= 2)
+                                ok = n == unit * S;
+                            CHECK(ok, "gemm ws M %d N %d K %d flags %#x: %zu", Ms[a], Ns[b], Ks[c], fl, n);
+                        }
+    }
+
     /* valid calls reach the runtime: without a device they must fail cleanly */
     const int rc = ATTN(vd_decode_attn, F, F, F, FI, FI, F, 4, 32, 8, 128, 16, 0.088f, 63, F, need, 0);
     CHECK(rc == VD_SUCCESS || rc == VD_ERROR_LAUNCH, "valid attn rc %d", rc);
