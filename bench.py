@@ -625,7 +625,7 @@ def layer_surface(outdir: str, reps: int = 5, batches=LAYER_BATCH, lengths=LAYER
     n_kv = np.array([r["n_kv"] for r in rows], float)
     t = np.array([r["us_layer"] for r in rows], float)
     fit = lm.fit_linear(n_req, n_kv, t)
-    bounds = (256, 512)
+    bounds = lm.tile_bounds(n_req)   # the coarse grid stops at 512: one edge, at 256
     tf = lm.fit_per_tile(n_req, n_kv, t, bounds)
     res = {"points": len(rows), "c_us_per_req": fit.c, "d_us_per_kv_token": fit.d, "e_us": fit.e,
            "r2": fit.r2, "mae_us": fit.mae,

@@ -121,6 +121,13 @@ class TileFit:
         return out
 
 
+def tile_bounds(n_req, candidates=(256, 512), min_points: int = 3) -> tuple:
+    """The band edges among `candidates` that a surface reaches past: an
+    edge is kept when at least `min_points` points lie above it."""
+    n_req = np.asarray(n_req, float)
+    return tuple(b for b in candidates if (n_req > b).sum() >= min_points)
+
+
 def fit_per_tile(n_req, n_kv, t, bounds=(256, 512)) -> TileFit:
     """Eq. pred-itl fitted separately in each band of N_req (see TileFit);
     every band needs points of its own."""
@@ -164,6 +171,9 @@ def holdout_mae(n_req, n_kv, t, test_fraction: float = 0.25, seed: int = 0, tile
     out = {"linear_mae_us": lin_mae, "boosted_mae_us": gb_mae, "n_train": int(tr.size),
            "n_test": int(te.size)}
     if tile_bounds is not None:
-        tf = fit_per_tile(n_req[tr], n_kv[tr], t[tr], tile_bounds)
-        out["tile_linear_mae_us"] = float(np.abs(tf.predict(n_req[te], n_kv[te]) - t[te]).mean())
+        try:
+            tf = fit_per_tile(n_req[tr], n_kv[tr], t[tr], tile_bounds)
+            out["tile_linear_mae_us"] = float(np.abs(tf.predict(n_req[te], n_kv[te]) - t[te]).mean())
+        except ValueError:   # the split left a band with too few training points
+            out["tile_linear_mae_us"] = None
     return out

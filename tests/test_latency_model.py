@@ -132,6 +132,13 @@ def test_per_tile_fit_follows_a_staircase():
     assert lm.fit_linear(n_req, n_kv, t).mae > 5
     with pytest.raises(ValueError):
         lm.fit_per_tile(n_req[n_req <= 300], n_kv[n_req <= 300], t[n_req <= 300], (256, 512))
+    # band edges follow the grid: none past 512 keeps only the edge at 256,
+    # and a held-out split that empties a band reports no per-band figure
+    sel = n_req <= 300
+    assert lm.tile_bounds(n_req[sel]) == (256,) and lm.tile_bounds(n_req) == (256, 512)
+    few = n_req <= 257
+    h = lm.holdout_mae(n_req[few], n_kv[few], t[few], test_fraction=0.5, seed=3, tile_bounds=(256,))
+    assert h["tile_linear_mae_us"] is None or h["tile_linear_mae_us"] >= 0
 
 
 def test_committed_dense_surface_shows_the_tile_steps():
