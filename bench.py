@@ -492,10 +492,10 @@ LAYER_BATCH = (1, 4, 16, 32, 64, 128, 192, 256, 384, 512)
 LAYER_LEN = (16, 64, 256, 1024, 4096)
 LAYER_RING = 4
 # the dense batch grid: both sides of the projection GEMMs' row-tile steps
-# (128 -> 160, 256 -> 257, 512 -> 513) at three lengths, layer time only
+# (128 -> 160, 256 -> 257, 512 -> 513) at six lengths, layer time only
 LAYER_DENSE_BATCH = (1, 32, 64, 96, 128, 144, 160, 192, 224, 240, 248, 255, 256, 257, 264, 272,
                      288, 320, 384, 448, 480, 496, 504, 511, 512, 513, 520, 528, 544, 576, 640)
-LAYER_DENSE_LEN = (64, 256, 1024)
+LAYER_DENSE_LEN = (64, 128, 256, 512, 1024, 2048)
 
 
 def layer_surface(outdir: str, reps: int = 5, batches=LAYER_BATCH, lengths=LAYER_LEN,

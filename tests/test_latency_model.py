@@ -144,7 +144,8 @@ def test_per_tile_fit_follows_a_staircase():
 def test_committed_dense_surface_shows_the_tile_steps():
     """The decode layer step measured on a dense batch grid (profiles/): it
     jumps where the projection GEMMs need another row tile (Sec. 3.3,
-    256 -> 257 and 512 -> 513) at every length, and Eq. pred-itl fitted per
+    256 -> 257 and 512 -> 513) at every length, by about the same time
+    (the GEMMs do not depend on the context), and Eq. pred-itl fitted per
     band between those boundaries predicts held-out points with well under
     half the error of one plane over all of them."""
     import csv
@@ -155,7 +156,7 @@ def test_committed_dense_surface_shows_the_tile_steps():
     assert len(rows) >= 80
     for L in {r["tokens_per_req"] for r in rows}:
         v = {int(r["n_req"]): float(r["us_layer"]) for r in rows if r["tokens_per_req"] == L}
-        assert v[257] > 1.05 * v[256] and v[513] > 1.05 * v[512]
+        assert v[257] - v[256] > 20 and v[513] - v[512] > 20          # us
         assert v[256] <= 1.02 * v[255] and v[512] <= 1.02 * v[511]   # no step before the boundary
     n_req, n_kv, t = lm.load_surface(path, n_q_heads=None, column="us_layer")
     tf = lm.fit_per_tile(n_req, n_kv, t, (256, 512))
