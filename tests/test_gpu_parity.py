@@ -16,7 +16,7 @@ import oracle
 import oracle_pins as pins
 import paper_2509_04827_amd as vd
 from parity_gates import CANARY_MAX_ABS, CANARY_REL_L2, GATE_MAX_ABS, GATE_REL_L2
-from workloads import ORDER, Workload, bits, make_case
+from workloads import ORDER, SHARDS, Workload, bits, make_case
 
 pytestmark = pytest.mark.gpu
 
@@ -87,7 +87,7 @@ def custom(lengths, hq=32, hkv=8, seed=0, fill="nan", shuffle=True, pt_stride=No
 
 
 # ------------------------------------------------------------------ workloads
-@pytest.mark.parametrize("name", ORDER)
+@pytest.mark.parametrize("name", ORDER + SHARDS)
 def test_workload_parity(name):
     say("case: workload %s seed 0" % name)
     c = make_case(name, seed=0, fill="nan")

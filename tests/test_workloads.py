@@ -3,7 +3,7 @@ the placement, page-table and fill rules of the recipe hold."""
 import numpy as np
 import torch
 
-from workloads import BF16_NAN_BITS, ORDER, WORKLOADS, bits, kv_bytes, make_case
+from workloads import BF16_NAN_BITS, ORDER, SHARDS, WORKLOADS, bits, kv_bytes, make_case
 
 
 def _same(a, b):
@@ -77,4 +77,16 @@ def test_identity_placement_and_sizes():
     assert flat.tolist() == list(range(int(P.sum())))
     assert kv_bytes(c) == 1665 * 8 * 128 * 2 * 2
     assert c["scale"] == float(np.float32(1 / np.sqrt(128)))
-    assert set(ORDER) == set(WORKLOADS)
+    assert set(ORDER) | set(SHARDS) == set(WORKLOADS) and not set(ORDER) & set(SHARDS)
+
+
+def test_tensor_parallel_shards_keep_the_requests():
+    """A shard is one GPU's share of gqa8_b128 with KV heads split over GPUs:
+    the same request lengths and page placement, Hkv / TP KV heads and the
+    query heads that read them (the group size G stays 8)."""
+    full = make_case("gqa8_b128", seed=0, fill="zero")
+    for name, tp in (("gqa8_b128_tp2", 2), ("gqa8_b128_tp8", 8)):
+        c = make_case(name, seed=0, fill="zero")
+        assert torch.equal(c["seq_lens"], full["seq_lens"]) and torch.equal(c["page_table"], full["page_table"])
+        assert c["n_kv_heads"] * tp == full["n_kv_heads"] and c["n_q_heads"] * tp == full["n_q_heads"]
+        assert kv_bytes(c) * tp == kv_bytes(full)

@@ -71,8 +71,17 @@ WORKLOADS = {
         "long_b16", 16, 32, 8, 128, 16, "loguniform", (1, 131072, 131072),
         description="long ragged: 16 requests, 32:8 heads, L_0 = 131072, "
                     "others log-uniform in [1,131072]"),
+    # one GPU's share of gqa8_b128 under tensor parallelism over KV heads:
+    # the same requests and lengths, Hkv / TP KV heads and their query heads
+    "gqa8_b128_tp2": Workload(
+        "gqa8_b128_tp2", 128, 32, 4, 128, 16, "uniform", (2048, 8192),
+        description="gqa8_b128 at TP = 2 (one GPU's share): 128 requests, 32:4 heads, L ~ U[2048,8192]"),
+    "gqa8_b128_tp8": Workload(
+        "gqa8_b128_tp8", 128, 8, 1, 128, 16, "uniform", (2048, 8192),
+        description="gqa8_b128 at TP = 8 (one GPU's share): 128 requests, 8:1 heads, L ~ U[2048,8192]"),
 }
 ORDER = ["tiny_b4", "llama8b_b64", "chat_b256", "gqa8_b128", "long_b16"]
+SHARDS = ["gqa8_b128_tp2", "gqa8_b128_tp8"]
 
 
 def _seed_of(ss: np.random.SeedSequence) -> int:
