@@ -840,6 +840,8 @@ def main():
     ap.add_argument("--clock-sweep", metavar="DIR", default=None,
                     help="instead of the bench line, time the attention kernel against the "
                          "shader clock it ran at and write DIR/decode_clock_sweep.{csv,json}")
+    ap.add_argument("--clock-bursts", type=int, default=10, metavar="N",
+                    help="with --clock-sweep: bursts of steps, each after an idle pause")
     ap.add_argument("--next-profile", metavar="DIR", default=None,
                     help="short run of the GEMM (4 shapes x M 1/16/64/256/257/1024) and KV-append kernels "
                          "for a kernel trace; writes next_profile.csv to DIR")
@@ -900,7 +902,7 @@ def main():
         gemm_sweep(args.gemm_sweep)
         return
     if args.clock_sweep:
-        clock_sweep(args.clock_sweep)
+        clock_sweep(args.clock_sweep, bursts=args.clock_bursts)
         return
     if args.cpu_configs:
         cpu_configs(args.cpu_configs)
